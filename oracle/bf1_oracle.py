@@ -1,0 +1,297 @@
+"""CPU oracle for BF1 causal dyadic block-sparse attention (prefill forward).
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import this module.  The product path
+(the HIP library and its Python binding) never imports, calls or links it,
+and this module imports nothing from the product path.
+
+Everything here is written for clarity, not speed: the route is enumerated
+as a set straight from its definition, the attention is an explicit masked
+softmax in float64, and no blocking, fusion or reordering is done beyond
+what the definition states.
+
+Notation (paper §3.1): a sequence of n tokens is cut into NB = ceil(n/b)
+blocks of width b, indexed 0..NB-1 (the paper calls the block count B; the
+C interface of the library uses B for the *width*, so this module writes
+b for the width and NB for the count to avoid the clash).
+
+Route (§3.1, Eq. 1): query block j selects
+    P(j) = {j, j-1, j-2, 0} ∪ {j - 2^r : r >= 2},
+with invalid (negative) and duplicate indices removed.  The paper's reported
+configuration has two local predecessor blocks; this oracle generalises the
+local part to {j-1, ..., j-L} for a local width L >= 0 and keeps the dyadic
+offsets at r >= 2 (offsets starting at four blocks, §3.1), so L = 2 is
+exactly Eq. 1.
+
+Mask (§3.1): the self block j uses a token-level causal triangle (key s is
+visible to query t in the same block iff s <= t); every other selected block
+is strictly earlier and fully visible.  Keys at positions >= n do not exist.
+
+Attention: softmax with scale 1/sqrt(head_dim) and no score bias (§3.1,
+"no scale-dependent score bias"), restricted to the mask above.  q-head h
+reads kv-head h // (Hq / Hkv) (contiguous GQA groups).  Outputs are O
+(same layout as Q) and the natural-log log-sum-exp LSE per query row.
+"""
+
+import math
+from collections import deque
+
+import numpy as np
+
+__all__ = [
+    "num_blocks",
+    "route",
+    "route_table",
+    "csr",
+    "token_mask",
+    "selected_pairs",
+    "dense_pairs",
+    "max_shortest_path",
+    "attn_full_mask_fp64",
+    "attn_gathered_fp64",
+    "attn_csr_fp64",
+    "dense_causal_fp64",
+]
+
+
+# ---------------------------------------------------------------------------
+# Route (§3.1, Eq. 1)
+# ---------------------------------------------------------------------------
+
+def num_blocks(n, b):
+    """NB = ceil(n / b) blocks of width b (§3.1)."""
+    if b <= 0:
+        raise ValueError("block width must be positive")
+    if n < 0:
+        raise ValueError("sequence length must be non-negative")
+    return (n + b - 1) // b
+
+
+def route(j, L=2):
+    """Selected key blocks of query block j, ascending (§3.1, Eq. 1).
+
+    The union of the self block, L local predecessors, the global first
+    block and the dyadic predecessors j - 2^r for r >= 2, with indices
+    outside [0, j] and duplicates removed.
+    """
+    if j < 0:
+        raise ValueError("block index must be non-negative")
+    if L < 0:
+        raise ValueError("local width must be non-negative")
+    chosen = {j, 0}
+    for ell in range(1, L + 1):
+        chosen.add(j - ell)
+    r = 2
+    while (1 << r) <= j:
+        chosen.add(j - (1 << r))
+        r += 1
+    return sorted(i for i in chosen if 0 <= i <= j)
+
+
+def route_table(n, b, L=2):
+    """List of routes, one per query block."""
+    return [route(j, L) for j in range(num_blocks(n, b))]
+
+
+def csr(n, b, L=2):
+    """Route as a CSR table: row_ptr[NB+1], col_idx[nnz] (int32, ascending)."""
+    rows = route_table(n, b, L)
+    row_ptr = np.zeros(len(rows) + 1, dtype=np.int64)
+    for j, r in enumerate(rows):
+        row_ptr[j + 1] = row_ptr[j] + len(r)
+    col_idx = np.array([i for r in rows for i in r], dtype=np.int64)
+    return row_ptr.astype(np.int32), col_idx.astype(np.int32)
+
+
+def token_mask(n, b, L=2, rows=None):
+    """Boolean token mask allowed[t, s] of shape [len(rows), n] (§3.1).
+
+    allowed(t, s) holds iff block(s) is in P(block(t)) and either block(s)
+    is strictly earlier than block(t) or s <= t inside the self block.
+    """
+    if rows is None:
+        rows = np.arange(n)
+    rows = np.asarray(rows)
+    allowed = np.zeros((len(rows), n), dtype=bool)
+    s = np.arange(n)
+    for a, t in enumerate(rows):
+        j = t // b
+        for i in route(j, L):
+            lo, hi = i * b, min((i + 1) * b, n)
+            if i < j:
+                allowed[a, lo:hi] = True
+            else:  # self block: token-level causal triangle, diagonal kept
+                allowed[a, lo:hi] = s[lo:hi] <= t
+    return allowed
+
+
+def selected_pairs(n, b, L=2):
+    """Selected (query, key) token pairs per (batch, head), by enumeration.
+
+    Walks every query block and every selected key block and counts the
+    visible pairs of that block pair: a full rectangle for an earlier block,
+    the causal triangle (diagonal included) for the self block.
+    """
+    total = 0
+    for j, sel in enumerate(route_table(n, b, L)):
+        rows_j = min((j + 1) * b, n) - j * b
+        for i in sel:
+            if i < j:
+                total += rows_j * (min((i + 1) * b, n) - i * b)
+            else:
+                total += rows_j * (rows_j + 1) // 2
+    return total
+
+
+def dense_pairs(n):
+    """Token pairs of dense causal attention, diagonal included."""
+    return n * (n + 1) // 2
+
+
+def max_shortest_path(NB, L=2):
+    """Largest shortest-path length, in layers, from any block to any later
+    block of the block graph whose edges are i -> j for i in P(j), i != j
+    (the communication depth of §3.3, Proposition 2).  Breadth-first search
+    from every source block."""
+    succ = [[] for _ in range(NB)]
+    for j in range(NB):
+        for i in route(j, L):
+            if i != j:
+                succ[i].append(j)
+    worst = 0
+    for src in range(NB):
+        dist = [-1] * NB
+        dist[src] = 0
+        queue = deque([src])
+        while queue:
+            u = queue.popleft()
+            for w in succ[u]:
+                if dist[w] < 0:
+                    dist[w] = dist[u] + 1
+                    queue.append(w)
+        for j in range(src + 1, NB):
+            if dist[j] < 0:
+                raise AssertionError(f"block {j} unreachable from {src}")
+            worst = max(worst, dist[j])
+    return worst
+
+
+# ---------------------------------------------------------------------------
+# Attention (§3.1 mask; softmax attention without bias)
+# ---------------------------------------------------------------------------
+
+def _check_shapes(q, k, v):
+    if q.ndim != 4 or k.ndim != 4 or v.ndim != 4:
+        raise ValueError("expected [batch, heads, n, head_dim] arrays")
+    batch, Hq, n, d = q.shape
+    if k.shape != v.shape or k.shape[0] != batch or k.shape[2] != n or k.shape[3] != d:
+        raise ValueError("K and V must be [batch, Hkv, n, head_dim] matching Q")
+    Hkv = k.shape[1]
+    if Hkv == 0 or Hq % Hkv != 0:
+        raise ValueError("Hq must be a multiple of Hkv")
+    return batch, Hq, Hkv, n, d
+
+
+def _softmax_rows(x, vals):
+    """Explicit softmax over the last axis of x (rows with -inf entries are
+    masked keys), returning (weights @ vals, log-sum-exp)."""
+    m = np.max(x, axis=-1, keepdims=True)
+    lse = m + np.log(np.sum(np.exp(x - m), axis=-1, keepdims=True))
+    w = np.exp(x - lse)
+    return w @ vals, lse[..., 0]
+
+
+def attn_full_mask_fp64(q, k, v, b, L=2, scale=None):
+    """Form (i): materialise the n x n token mask and run a masked softmax.
+
+    For small n only (memory is n^2 per head).  Inputs are float arrays in
+    [batch, H, n, d] layout; returns (O float64 [batch, Hq, n, d],
+    LSE float64 [batch, Hq, n], natural log).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    batch, Hq, Hkv, n, d = _check_shapes(q, k, v)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    G = Hq // Hkv
+    mask = token_mask(n, b, L)
+    out = np.zeros((batch, Hq, n, d))
+    lse = np.zeros((batch, Hq, n))
+    for beta in range(batch):
+        for h in range(Hq):
+            g = h // G
+            x = scale * (q[beta, h] @ k[beta, g].T)
+            x = np.where(mask, x, -np.inf)
+            out[beta, h], lse[beta, h] = _softmax_rows(x, v[beta, g])
+    return out, lse
+
+
+def attn_csr_fp64(q, k, v, b, row_ptr, col_idx, scale=None, blocks=None):
+    """Form (ii): gathered attention over an explicit block route given as
+    a CSR table (row j selects key blocks col_idx[row_ptr[j]:row_ptr[j+1]]).
+
+    Per query block, the selected key ranges are concatenated, the self
+    block gets its causal triangle, and one explicit softmax runs over the
+    gathered keys.  ``blocks`` restricts the computation to some query
+    blocks (the other rows of the outputs are left as NaN).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    batch, Hq, Hkv, n, d = _check_shapes(q, k, v)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    G = Hq // Hkv
+    NB = num_blocks(n, b)
+    out = np.full((batch, Hq, n, d), np.nan)
+    lse = np.full((batch, Hq, n), np.nan)
+    todo = range(NB) if blocks is None else blocks
+    for j in todo:
+        t0, t1 = j * b, min((j + 1) * b, n)
+        sel = [int(i) for i in col_idx[row_ptr[j]:row_ptr[j + 1]]]
+        keys = np.concatenate([np.arange(i * b, min((i + 1) * b, n)) for i in sel])
+        t = np.arange(t0, t1)[:, None]
+        s = keys[None, :]
+        allowed = (s // b < j) | (s <= t)
+        for beta in range(batch):
+            for h in range(Hq):
+                g = h // G
+                x = scale * (q[beta, h, t0:t1] @ k[beta, g, keys].T)
+                x = np.where(allowed, x, -np.inf)
+                out[beta, h, t0:t1], lse[beta, h, t0:t1] = _softmax_rows(x, v[beta, g, keys])
+    return out, lse
+
+
+def attn_gathered_fp64(q, k, v, b, L=2, scale=None, blocks=None):
+    """Form (ii) over the BF1 route of Eq. 1 (O(n log n) work)."""
+    n = np.shape(q)[2]
+    row_ptr, col_idx = csr(n, b, L)
+    return attn_csr_fp64(q, k, v, b, row_ptr, col_idx, scale=scale, blocks=blocks)
+
+
+def dense_causal_fp64(q, k, v, scale=None, rows=None):
+    """Plain dense causal softmax attention in float64 (every key s <= t).
+
+    ``rows`` optionally restricts the query positions computed (others NaN).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    batch, Hq, Hkv, n, d = _check_shapes(q, k, v)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    G = Hq // Hkv
+    rows = np.arange(n) if rows is None else np.asarray(rows)
+    out = np.full((batch, Hq, n, d), np.nan)
+    lse = np.full((batch, Hq, n), np.nan)
+    for beta in range(batch):
+        for h in range(Hq):
+            g = h // G
+            for t in rows:
+                x = scale * (k[beta, g, : t + 1] @ q[beta, h, t])
+                m = np.max(x)
+                z = np.sum(np.exp(x - m))
+                lse[beta, h, t] = m + np.log(z)
+                out[beta, h, t] = np.exp(x - lse[beta, h, t]) @ v[beta, g, : t + 1]
+    return out, lse

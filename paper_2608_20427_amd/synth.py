@@ -1,0 +1,99 @@
+"""Seeded synthetic inputs for BF1 attention.
+
+This module only draws random tensors.  It holds none of the attention
+arithmetic, and it is the one module that both the HIP path's tests and the
+CPU oracle's tests take their inputs from: the same bf16 bits go to the GPU
+and (converted exactly to float64) to the oracle.
+
+Recipe: a NumPy ``Generator(PCG64(seed))`` draws Q, then K, then V as float32
+standard normals in [batch, heads, n, head_dim] order; each tensor is
+rounded to bf16 (round-to-nearest-even) by PyTorch on the CPU.  The peaked
+workload additionally multiplies K by a factor at a random 5% of the token
+positions of each batch element (all kv-heads, all dims), in float32 before
+the bf16 rounding, so that some softmax rows are dominated by a few keys.
+
+The workloads follow the paper's evaluated attention geometry (Qwen3-0.6B:
+16 query heads, 8 kv-heads, head dimension 128, block width 64 and two local
+blocks, §3.1 and §4.1); the paper's model activations and corpus are not
+available, so seeded normals of that exact shape stand in for them.
+"""
+
+from dataclasses import dataclass, field, replace
+
+import numpy as np
+import torch
+
+__all__ = ["Workload", "WORKLOADS", "sweep", "make_qkv", "to_f64"]
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    batch: int
+    n: int
+    Hq: int
+    Hkv: int
+    d: int
+    b: int
+    L: int
+    seed: int
+    peak_frac: float = 0.0  # fraction of token positions whose K is scaled
+    peak_mul: float = 3.0
+    note: str = field(default="", compare=False)
+
+    def with_(self, **kw):
+        return replace(self, **kw)
+
+
+# The named workloads: a tiny case, the Qwen3-0.6B layer geometry at 4K and
+# at 32K (the headline point), and a batched case with a partial final block
+# (30001 = 468 * 64 + 49) and peaked rows.
+WORKLOADS = {
+    "tiny_n512": Workload("tiny_n512", 1, 512, 2, 1, 64, 64, 1, 0,
+                          note="tiny: batch 1, n=512, Hq=2, Hkv=1, d=64, b=64, L=1"),
+    "qwen_n4096": Workload("qwen_n4096", 1, 4096, 16, 8, 128, 64, 2, 1,
+                           note="Qwen3-0.6B layer geometry, n=4096"),
+    "qwen_n32768": Workload("qwen_n32768", 1, 32768, 16, 8, 128, 64, 2, 2,
+                            note="Qwen3-0.6B layer geometry, n=32768"),
+    "qwen_n30001_b2_peaked": Workload("qwen_n30001_b2_peaked", 2, 30001, 16, 8, 128, 64, 2, 3,
+                                      peak_frac=0.05, peak_mul=3.0,
+                                      note="batch 2, n=30001 (partial last block), K x3 on 5% of positions"),
+}
+
+
+def sweep(b=64):
+    """The length sweep 1K..64K in the Qwen3-0.6B geometry, seed 1000+log2(n)."""
+    out = []
+    for lg in range(10, 17):
+        n = 1 << lg
+        out.append(Workload(f"sweep_n{n}_b{b}", 1, n, 16, 8, 128, b, 2, 1000 + lg,
+                            note=f"sweep point n={n}, b={b}"))
+    return out
+
+
+def make_qkv(w, device="cpu"):
+    """Draw Q, K, V for workload ``w`` as bf16 torch tensors.
+
+    Q: [batch, Hq, n, d]; K, V: [batch, Hkv, n, d].  Drawing happens on the
+    host so that the bits do not depend on the device.
+    """
+    rng = np.random.Generator(np.random.PCG64(w.seed))
+    q = rng.standard_normal((w.batch, w.Hq, w.n, w.d), dtype=np.float32)
+    k = rng.standard_normal((w.batch, w.Hkv, w.n, w.d), dtype=np.float32)
+    v = rng.standard_normal((w.batch, w.Hkv, w.n, w.d), dtype=np.float32)
+    if w.peak_frac > 0.0 and w.n > 0:
+        count = int(round(w.peak_frac * w.n))
+        for beta in range(w.batch):
+            pos = rng.choice(w.n, size=count, replace=False)
+            k[beta, :, pos, :] *= np.float32(w.peak_mul)
+    tq = torch.from_numpy(q).to(torch.bfloat16)
+    tk = torch.from_numpy(k).to(torch.bfloat16)
+    tv = torch.from_numpy(v).to(torch.bfloat16)
+    if device != "cpu":
+        tq, tk, tv = tq.to(device), tk.to(device), tv.to(device)
+    return tq, tk, tv
+
+
+def to_f64(t):
+    """Exact float64 copy of a bf16 tensor as a NumPy array."""
+    return t.detach().to("cpu").to(torch.float64).numpy()

@@ -1,0 +1,118 @@
+"""Planted mistakes in the oracle (CPU only): each plausible slip -- a dropped
+route term, a wrong offset, a strict diagonal, a wrong scale, a wrong GQA map,
+a dropped log-sum-exp term -- must make at least one pin fail.  This checks
+that the pins are sharp enough to trust the oracle."""
+
+import numpy as np
+import pytest
+
+import test_oracle_attention as TA
+import test_oracle_route as TR
+from oracle import bf1_oracle as orc
+
+_route = orc.route
+
+
+def route_no_global(j, L=2):
+    return [i for i in _route(j, L) if i != 0 or j == 0]
+
+
+def route_dyadic_from_8(j, L=2):
+    out = set(_route(j, L))
+    if j >= 4 and 4 > L:
+        out.discard(j - 4)
+    return sorted(out)
+
+
+def route_extra_j3(j, L=2):
+    out = set(_route(j, L))
+    if j >= 3:
+        out.add(j - 3)
+    return sorted(out)
+
+
+def run_pins(pins):
+    """Return True if some pin fails under the current (mutated) oracle."""
+    for fn, args in pins:
+        try:
+            fn(*args)
+        except AssertionError:
+            return True
+    return False
+
+
+ROUTE_PINS = [
+    (TR.test_route_matches_hand_derived_eq1, ()),
+    (TR.test_interaction_reduction_32k, ()),
+    (TR.test_pairs_brute_force, (777, 2)),
+]
+
+
+@pytest.mark.parametrize("bad", [route_no_global, route_dyadic_from_8, route_extra_j3])
+def test_route_mutations_are_caught(monkeypatch, bad):
+    monkeypatch.setattr(orc, "route", bad)
+    assert run_pins(ROUTE_PINS)
+
+
+def softmax_no_max_shift_in_lse(x, vals):
+    m = np.max(x, axis=-1, keepdims=True)
+    lse = np.log(np.sum(np.exp(x - m), axis=-1, keepdims=True))   # forgot "+ m"
+    w = np.exp(x - m - lse)
+    return w @ vals, lse[..., 0]
+
+
+def softmax_unnormalised(x, vals):
+    m = np.max(x, axis=-1, keepdims=True)
+    w = np.exp(x - m)
+    return w @ vals, (m + np.log(np.sum(w, axis=-1, keepdims=True)))[..., 0]
+
+
+ATTN_PINS = [
+    (TA.test_oracle_equals_library_sdpa_on_hand_mask, (70, 4)),
+    (TA.test_route_covering_every_block_is_dense_causal, (256, 64, 2)),
+    (TA.test_zero_keys_closed_form, (777, 64, 2)),
+    (TA.test_gqa_grouping_contiguous, ()),
+]
+
+
+@pytest.mark.parametrize("bad", [softmax_no_max_shift_in_lse, softmax_unnormalised])
+def test_softmax_mutations_are_caught(monkeypatch, bad):
+    monkeypatch.setattr(orc, "_softmax_rows", bad)
+    assert run_pins(ATTN_PINS)
+
+
+def test_strict_diagonal_is_caught(monkeypatch):
+    real = orc.token_mask
+
+    def strict(n, b, L=2, rows=None):
+        m = real(n, b, L, rows)
+        r = np.arange(n) if rows is None else np.asarray(rows)
+        m[np.arange(len(r)), r] = False
+        return m
+
+    monkeypatch.setattr(orc, "token_mask", strict)
+    assert run_pins([(TR.test_pairs_brute_force, (257, 2)), (TR.test_mask_is_causal_and_keeps_diagonal, ())])
+
+
+def test_wrong_scale_is_caught(monkeypatch):
+    real = orc.attn_csr_fp64
+    monkeypatch.setattr(orc, "attn_csr_fp64",
+                        lambda q, k, v, b, rp, ci, scale=None, blocks=None:
+                        real(q, k, v, b, rp, ci, scale=1.0 / q.shape[-1], blocks=blocks))
+    assert run_pins(ATTN_PINS)
+
+
+def test_wrong_gqa_map_is_caught(monkeypatch):
+    real = orc.attn_csr_fp64
+
+    def interleaved(q, k, v, b, rp, ci, scale=None, blocks=None):
+        # maps q-head h to kv-head h % Hkv instead of h // G
+        Hq, Hkv = q.shape[1], k.shape[1]
+        G = Hq // Hkv
+        idx = [h % Hkv for h in range(Hq)]
+        kk = np.repeat(k, 1, axis=1)[:, idx]
+        vv = np.repeat(v, 1, axis=1)[:, idx]
+        return real(q, kk, vv, b, rp, ci, scale=scale, blocks=blocks) if G > 1 else real(q, k, v, b, rp, ci, scale, blocks)
+
+    monkeypatch.setattr(orc, "attn_csr_fp64", interleaved)
+    assert run_pins([(TA.test_gqa_grouping_contiguous, ())])
