@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Benchmark of the BF1 prefill forward on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--sweep]
+
+A step is one pass of the whole hot path over one batch of synthetic input
+already resident in HBM: the route planner writes the CSR table, then the
+attention kernel walks it (bf1_plan + bf1_attn_fwd_csr on one stream).  The
+timed region is exactly K steps bracketed by device synchronisation.  The
+default workload is the Qwen3-0.6B layer geometry at n = 32768 (batch 1,
+16 q-heads, 8 kv-heads, head_dim 128, block width 64, two local blocks).
+
+The last line of stdout is one JSON record:
+  value      selected-interaction TFLOP/s of the whole step
+             (4 * head_dim * selected pairs * Hq * batch / step time)
+  roofline   the attention kernel alone: achieved TFLOP/s (HIP events on its
+             stream, averaged over the K timed launches) against the
+             published dense bf16 MFMA peak of MI355X (2.5 PFLOP/s)
+  dense      the in-house dense causal kernel timed with the paper's
+             protocol (5 warmups, 30 reps, two opposite orders, median of the
+             two order medians, §4.3) next to BF1 timed the same way
+  cpu_baseline  the fp64 CPU oracle on a bounded sample of the workload
+
+--sweep additionally times n = 1K..64K for block widths 64 and 128 with the
+two-order protocol and writes one JSON record per point to --sweep-out.
+"""
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X published dense bf16 MFMA peak
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen_n32768")
+    ap.add_argument("--reps", type=int, default=30, help="reps per order in the two-order protocol")
+    ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--sweep-out", default=os.path.join(ROOT, "gpurun_out", "sweep.jsonl"))
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="time bound of the CPU oracle sample")
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "bf1_fwd_traffic.json"))
+    return ap.parse_args()
+
+
+def timed_reps(torch, fn, warmup, reps):
+    """Per-launch device times (ms) of fn on the current stream."""
+    for _ in range(warmup):
+        fn()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in ev:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
+def two_order(torch, fa, fb, warmup, reps):
+    """Paper protocol (§4.3): both orders, median of the two order medians."""
+    a1 = timed_reps(torch, fa, warmup, reps)
+    b1 = timed_reps(torch, fb, warmup, reps)
+    b2 = timed_reps(torch, fb, warmup, reps)
+    a2 = timed_reps(torch, fa, warmup, reps)
+
+    def summ(x, y):
+        allv = sorted(x + y)
+        return {"ms": statistics.median([statistics.median(x), statistics.median(y)]),
+                "p10": allv[int(0.1 * (len(allv) - 1))], "p90": allv[int(0.9 * (len(allv) - 1))]}
+    return summ(a1, a2), summ(b1, b2)
+
+
+def cpu_baseline(w, max_seconds):
+    """The fp64 oracle on a bounded sample of the workload: query blocks in
+    an evenly spread order (heaviest first), 16 at a time, until the time
+    bound is reached or the whole workload is done."""
+    from oracle import bf1_oracle as orc
+    from paper_2608_20427_amd import synth
+    q, k, v = synth.make_qkv(w)
+    qd, kd, vd = synth.to_f64(q), synth.to_f64(k), synth.to_f64(v)
+    NB = orc.num_blocks(w.n, w.b)
+    order = []
+    for stride_off in range(8):
+        order.extend(range(NB - 1 - stride_off, -1, -8))
+    rp, ci = orc.csr(w.n, w.b, w.L)
+    pairs, done = 0, []
+    t0 = time.perf_counter()
+    for at in range(0, len(order), 16):
+        chunk = order[at:at + 16]
+        orc.attn_gathered_fp64(qd, kd, vd, w.b, w.L, blocks=chunk)
+        done.extend(chunk)
+        if time.perf_counter() - t0 > max_seconds:
+            break
+    dt = time.perf_counter() - t0
+    for j in done:
+        rows = min((j + 1) * w.b, w.n) - j * w.b
+        earlier = sum(min((int(i) + 1) * w.b, w.n) - int(i) * w.b
+                      for i in ci[rp[j]:rp[j + 1]] if int(i) < j)
+        pairs += rows * earlier + rows * (rows + 1) // 2
+    flops = 4 * w.d * int(pairs) * w.Hq * w.batch
+    cores = len(os.sched_getaffinity(0))
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "seconds": dt, "gflop": flops / 1e9,
+            "sample": f"{len(done)} of {NB} query blocks (strided order, heaviest first; whole "
+                      f"workload if under {max_seconds:.0f} s), all {w.Hq} q-heads, batch {w.batch}, "
+                      f"workload {w.name}; fp64 NumPy gathered oracle, BLAS threads = host cores"}
+
+
+def run_point(torch, bf1, w, q, k, v, warmup, reps, with_dense=True):
+    """Two-order timing of BF1 and dense on one workload."""
+    o = torch.empty_like(q)
+    lse = torch.empty((w.batch, w.Hq, w.n), dtype=torch.float32, device="cuda")
+    rp, ci = bf1.plan(w.n, w.b, w.L)
+    f_bf1 = lambda: bf1.attn_fwd_csr(q, k, v, w.b, rp, ci, out=o, lse=lse)
+    f_dense = lambda: bf1.dense_causal_fwd(q, k, v, out=o, lse=lse)
+    flops = bf1.selected_flops(w.batch, w.n, w.Hq, w.d, w.b, w.L)
+    dense_flops = 4 * w.d * (w.n * (w.n + 1) // 2) * w.Hq * w.batch
+    plan_ms = statistics.median(timed_reps(torch, lambda: bf1.plan(w.n, w.b, w.L, rp, ci), 3, 20))
+    if with_dense:
+        sb, sd = two_order(torch, f_bf1, f_dense, warmup, reps)
+    else:
+        x = timed_reps(torch, f_bf1, warmup, reps)
+        sb, sd = {"ms": statistics.median(x), "p10": min(x), "p90": max(x)}, None
+    rec = {"workload": w.name, "n": w.n, "b": w.b, "L": w.L, "batch": w.batch, "Hq": w.Hq,
+           "Hkv": w.Hkv, "head_dim": w.d, "selected_gflop": flops / 1e9,
+           "bf1_ms": sb["ms"], "bf1_p10_ms": sb["p10"], "bf1_p90_ms": sb["p90"],
+           "bf1_tflops": flops / sb["ms"] / 1e9,
+           "bf1_pct_peak": 100 * flops / sb["ms"] / 1e9 / PEAK_BF16_TFLOPS,
+           "plan_us": plan_ms * 1e3}
+    if sd is not None:
+        rec.update({"dense_gflop": dense_flops / 1e9, "dense_ms": sd["ms"], "dense_p10_ms": sd["p10"],
+                    "dense_p90_ms": sd["p90"], "dense_tflops": dense_flops / sd["ms"] / 1e9,
+                    "dense_pct_peak": 100 * dense_flops / sd["ms"] / 1e9 / PEAK_BF16_TFLOPS,
+                    "speedup_vs_dense": sd["ms"] / sb["ms"],
+                    "pair_reduction": dense_flops / flops})
+    return rec
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2608_20427_amd as bf1
+    from paper_2608_20427_amd import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    bf1.load()
+    w = synth.WORKLOADS[args.workload]
+    props = torch.cuda.get_device_properties(0)
+    log(f"device {props.name} CUs={props.multi_processor_count}; workload {w}")
+    q, k, v = synth.make_qkv(w, device="cuda")
+    NB, nnz, pairs = bf1.plan_size(w.n, w.b, w.L)
+    rp = torch.empty(NB + 1, dtype=torch.int32, device="cuda")
+    ci = torch.empty(nnz, dtype=torch.int32, device="cuda")
+    o = torch.empty_like(q)
+    lse = torch.empty((w.batch, w.Hq, w.n), dtype=torch.float32, device="cuda")
+    flops = bf1.selected_flops(w.batch, w.n, w.Hq, w.d, w.b, w.L)
+
+    def plan():
+        bf1.plan(w.n, w.b, w.L, rp, ci)
+
+    def attn():
+        bf1.attn_fwd_csr(q, k, v, w.b, rp, ci, out=o, lse=lse)
+
+    for _ in range(args.warmup):
+        plan()
+        attn()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    # ---- timed region: exactly K steps -------------------------------------
+    marks = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in marks:
+        plan()
+        a.record()
+        attn()
+        b.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = [a.elapsed_time(b) for a, b in marks]
+    ms_per_step = wall * 1e3 / args.steps
+    attn_ms = statistics.mean(kern_ms)
+    log(f"timed {args.steps} steps: {ms_per_step:.4f} ms/step, attention kernel {attn_ms:.4f} ms")
+
+    achieved = flops / (attn_ms * 1e-3) / 1e12
+    traffic = None
+    if os.path.exists(args.traffic_json):
+        try:
+            t = json.load(open(args.traffic_json))
+            if t.get("workload") == w.name:
+                traffic = t.get("bytes_per_launch")
+        except (OSError, ValueError):
+            traffic = None
+    rec = {
+        "metric": "BF1 prefill per-layer ms and selected-pair TFLOP/s (% MFMA peak) vs dense, 1K-64K",
+        "value": flops / (ms_per_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "seq_len": w.n, "Hq": w.Hq, "Hkv": w.Hkv,
+                   "head_dim": w.d, "block_width": w.b, "local_blocks": w.L,
+                   "parallelism": "none (one GPU)"},
+        "per_layer_ms": ms_per_step,
+        "selected_gflop": flops / 1e9,
+        "pct_mfma_peak": 100 * achieved / PEAK_BF16_TFLOPS,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
+                     "kernel": "attn_fwd_kernel<128,2,64,4,false>",
+                     "kernel_ms": attn_ms},
+    }
+
+    if not args.no_dense:
+        point = run_point(torch, bf1, w, q, k, v, args.warmup, args.reps)
+        rec["paper_protocol"] = point
+        log(f"two-order protocol: bf1 {point['bf1_ms']:.4f} ms, dense {point.get('dense_ms', 0):.4f} ms,"
+            f" speedup {point.get('speedup_vs_dense', 0):.2f}x")
+
+    if args.sweep:
+        os.makedirs(os.path.dirname(args.sweep_out), exist_ok=True)
+        with open(args.sweep_out, "w") as f:
+            for b in (64, 128):
+                for sw in synth.sweep(b):
+                    sq, sk, sv = synth.make_qkv(sw, device="cuda")
+                    r = run_point(torch, bf1, sw, sq, sk, sv, 5, 30)
+                    f.write(json.dumps(r) + "\n")
+                    f.flush()
+                    log(f"sweep n={sw.n} b={b}: bf1 {r['bf1_ms']:.4f} ms ({r['bf1_tflops']:.1f} TF/s,"
+                        f" {r['bf1_pct_peak']:.1f}%), dense {r['dense_ms']:.4f} ms"
+                        f" ({r['dense_tflops']:.1f} TF/s), speedup {r['speedup_vs_dense']:.2f}x")
+                    del sq, sk, sv
+
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        rec["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        log(f"cpu baseline {rec['cpu_baseline']['value'] * 1e3:.3f} GFLOP/s in "
+            f"{rec['cpu_baseline']['seconds']:.1f} s")
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,136 @@
+/*
+ * bf1.h -- C interface of libbf1.so: BF1 causal dyadic block-sparse
+ * attention, prefill forward, for AMD Instinct MI355X (gfx950).
+ *
+ * The operation (paper §3.1, Eq. 1).  A sequence of n tokens is cut into
+ * NB = ceil(n / B) blocks of B tokens (B is the block WIDTH here; the paper
+ * writes b for the width and B for the count).  Query block j attends to the
+ * key blocks
+ *     P(j) = {j} ∪ {j-1, ..., j-L} ∪ {0} ∪ {j - 2^r : r >= 2},
+ * restricted to [0, j] with duplicates removed (L = 2 is the paper's
+ * configuration: two local blocks, the global first block, dyadic offsets
+ * starting at four blocks).  Inside the self block j a token-level causal
+ * triangle applies (key s visible to query t iff s <= t); every other selected
+ * block is strictly earlier and fully visible.  Attention is softmax with
+ * scale 1/sqrt(head_dim) and no bias (§3.1).  The result is exact softmax
+ * attention restricted to that token mask (O(n log n) pairs, §3.2 Prop. 1).
+ *
+ * Conventions shared by every entry point:
+ *  - All functions have C linkage, never abort or exit, and are thread-safe.
+ *  - Device work is enqueued asynchronously on `stream` (a hipStream_t; NULL
+ *    is the default stream of the current device).  Errors raised by the
+ *    device surface at the caller's next synchronisation.
+ *  - Argument errors are returned before anything is enqueued; no output is
+ *    written in that case.
+ *  - All tensors are caller-owned device memory on the current device.  The
+ *    library never frees caller memory; it owns only its plan cache.
+ *  - Layouts (row-major, contiguous):
+ *        Q, O : [batch, Hq,  n, head_dim] bf16
+ *        K, V : [batch, Hkv, n, head_dim] bf16
+ *        LSE  : [batch, Hq,  n]           fp32, natural log of the softmax
+ *                                           denominator including the max
+ *    Q, K, V, O must be 16-byte aligned; LSE 4-byte aligned.
+ *    q-head h reads kv-head h / (Hq / Hkv) (contiguous GQA groups).
+ *  - Supported by the attention kernels: head_dim in {64, 128},
+ *    B in {64, 128}, Hq / Hkv in {1, 2, 4, 8}, L >= 0, n >= 0, batch >= 0.
+ *    Other values return BF1_ERR_UNSUPPORTED.  n == 0 or batch == 0 is a
+ *    no-op returning BF1_OK.
+ */
+#ifndef BF1_H
+#define BF1_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BF1_OK = 0,
+    BF1_ERR_INVALID_ARG = -1,      /* null pointer, misalignment, bad size */
+    BF1_ERR_UNSUPPORTED = -2,      /* valid but not built: head_dim, B, group */
+    BF1_ERR_BUFFER_TOO_SMALL = -3, /* col_capacity below the route size */
+    BF1_ERR_HIP = -4,              /* a HIP runtime call or launch failed */
+    BF1_ERR_NOMEM = -5             /* device allocation for the plan cache failed */
+} bf1_status;
+
+/*
+ * Route sizes in closed form (host only, no device work).  §3.1 Eq. 1 for
+ * the route and §3.2 Prop. 1 for the O(n log n) pair law.
+ *   n >= 0, B >= 1, L >= 0.
+ *   num_blocks <- NB = ceil(n / B)
+ *   nnz        <- total entries of the CSR table (sum over j of |P(j)|)
+ *   pairs      <- selected (query, key) token pairs per (batch, head),
+ *                 counting the self-block triangle with its diagonal and a
+ *                 partial last block of n - (NB-1)*B tokens.
+ * Any output pointer may be NULL.  Returns BF1_ERR_INVALID_ARG on bad sizes
+ * or if nnz would not fit in int32 indices.
+ */
+int bf1_plan_size(int64_t n, int32_t B, int32_t L,
+                  int32_t* num_blocks, int64_t* nnz, int64_t* pairs);
+
+/*
+ * Route planner (§3.1, Eq. 1): writes the selected key-block table as CSR.
+ *   row_ptr : device int32[NB + 1]; row_ptr[0] = 0, row_ptr[NB] = nnz.
+ *   col_idx : device int32[col_capacity]; row j holds P(j) in ascending
+ *             order (the self block j last), entries row_ptr[j]..row_ptr[j+1].
+ * One integer HIP kernel, asynchronous on `stream`.  Returns
+ * BF1_ERR_BUFFER_TOO_SMALL (nothing enqueued) if col_capacity < nnz.
+ * n >= 0, B >= 1, L >= 0; n == 0 writes row_ptr[0] = 0 only.
+ */
+int bf1_plan(int64_t n, int32_t B, int32_t L,
+             int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity,
+             void* stream);
+
+/*
+ * BF1 prefill forward (§3.1): O and LSE for every (batch, q-head, token).
+ * The route is built by the planner on first use for (device, n, B, L) and
+ * kept in a library-owned cache (see bf1_release_plans); the attention
+ * kernel then walks only the selected key blocks of each query block.
+ * LSE may be NULL (not written).
+ */
+int bf1_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                 int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                 int32_t B, int32_t L, void* stream);
+
+/*
+ * The same kernel with a caller-supplied route table (any block route in
+ * the CSR form written by bf1_plan; used for route variants and tests).
+ *   row_ptr : device int32[ceil(n/B) + 1], non-decreasing.
+ *   col_idx : device int32[nnz]; entries of row j name key blocks.
+ * Row ranges are clamped to [0, nnz]; entries outside [0, j] are ignored
+ * (the route is causal: the self block j gets the token-level triangle,
+ * earlier blocks are fully visible).  Each block should appear at most once
+ * per row, and rows that name no block at all produce undefined values (never
+ * an out-of-bounds access).  All memory stays caller-owned.
+ */
+int bf1_attn_fwd_csr(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                     int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                     int32_t B, const int32_t* row_ptr, const int32_t* col_idx, int64_t nnz,
+                     void* stream);
+
+/*
+ * Dense causal attention (every key s <= t), built from the same kernel with
+ * the implicit route {0, ..., j} over 64-token blocks: the in-run comparator
+ * for the BF1 operator (the paper compares against dense attention, §4.3).
+ * Same layouts and support set as bf1_attn_fwd (no B, L).
+ */
+int bf1_dense_causal_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                         int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                         void* stream);
+
+/* Frees every cached plan (device memory owned by the library).  Must not
+ * race with in-flight bf1_attn_fwd calls that use those plans. */
+void bf1_release_plans(void);
+
+/* Static, human-readable name of a status code. */
+const char* bf1_status_string(int status);
+
+/* Interface version (major * 10000 + minor * 100 + patch). */
+int bf1_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BF1_H */

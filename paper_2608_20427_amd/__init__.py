@@ -1,1 +1,187 @@
-"""BF1 causal dyadic block-sparse attention for MI355X (gfx950)."""
+"""BF1 causal dyadic block-sparse attention (prefill forward) for MI355X.
+
+Thin ctypes binding over libbf1.so (declared in include/bf1.h).  Every
+function here only checks tensor metadata and marshals pointers, sizes and
+the current HIP stream; every step of the computation runs in the library's
+HIP kernels.  There is no fallback: if the library is not built, or a call
+fails, an exception is raised.
+
+Layouts: Q, O [batch, Hq, n, d] bf16; K, V [batch, Hkv, n, d] bf16;
+LSE [batch, Hq, n] float32 (natural log).  q-head h reads kv-head
+h // (Hq // Hkv).  Block width ``B`` (tokens per block) and local width
+``L`` (blocks) define the route of the paper's §3.1, Eq. 1.
+"""
+
+import ctypes
+import os
+
+__all__ = [
+    "BF1Error", "lib_path", "load", "version", "status_string", "plan_size", "plan",
+    "attn_fwd", "attn_fwd_csr", "dense_causal_fwd", "release_plans", "selected_flops",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+BF1_OK = 0
+BF1_ERR_INVALID_ARG = -1
+BF1_ERR_UNSUPPORTED = -2
+BF1_ERR_BUFFER_TOO_SMALL = -3
+BF1_ERR_HIP = -4
+BF1_ERR_NOMEM = -5
+
+
+class BF1Error(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+
+
+def lib_path():
+    return os.path.join(_HERE, "libbf1.so")
+
+
+def load():
+    """Load libbf1.so (built in-tree by __graft_entry__.build()).  Raises if
+    it is missing: there is no other implementation to fall back to."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = lib_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run `python -m paper_2608_20427_amd.build`")
+    lib = ctypes.CDLL(path)
+    i32, i64, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+    lib.bf1_version.restype = ctypes.c_int
+    lib.bf1_version.argtypes = []
+    lib.bf1_status_string.restype = ctypes.c_char_p
+    lib.bf1_status_string.argtypes = [ctypes.c_int]
+    lib.bf1_plan_size.restype = ctypes.c_int
+    lib.bf1_plan_size.argtypes = [i64, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i64),
+                                  ctypes.POINTER(i64)]
+    lib.bf1_plan.restype = ctypes.c_int
+    lib.bf1_plan.argtypes = [i64, i32, i32, vp, vp, i64, vp]
+    attn = [vp, vp, vp, vp, vp, i32, i64, i32, i32, i32]
+    lib.bf1_attn_fwd.restype = ctypes.c_int
+    lib.bf1_attn_fwd.argtypes = attn + [i32, i32, vp]
+    lib.bf1_attn_fwd_csr.restype = ctypes.c_int
+    lib.bf1_attn_fwd_csr.argtypes = attn + [i32, vp, vp, i64, vp]
+    lib.bf1_dense_causal_fwd.restype = ctypes.c_int
+    lib.bf1_dense_causal_fwd.argtypes = attn + [vp]
+    lib.bf1_release_plans.restype = None
+    lib.bf1_release_plans.argtypes = []
+    _LIB = lib
+    return lib
+
+
+def _check(status, where):
+    if status != BF1_OK:
+        raise BF1Error(status, where)
+
+
+def version():
+    return load().bf1_version()
+
+
+def status_string(status):
+    return load().bf1_status_string(int(status)).decode()
+
+
+def plan_size(n, B=64, L=2):
+    """(num_blocks, nnz, selected pairs per (batch, head)) in closed form."""
+    nb, nnz, pairs = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64()
+    _check(load().bf1_plan_size(int(n), int(B), int(L), ctypes.byref(nb), ctypes.byref(nnz),
+                                ctypes.byref(pairs)), "bf1_plan_size")
+    return nb.value, nnz.value, pairs.value
+
+
+def selected_flops(batch, n, Hq, d, B=64, L=2):
+    """Algorithmic flops of the forward: 4 d per selected pair (QK^T and PV),
+    per q-head and batch element."""
+    return 4 * d * plan_size(n, B, L)[2] * Hq * batch
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def plan(n, B=64, L=2, row_ptr=None, col_idx=None, stream=None):
+    """Route table of Eq. 1 as device CSR (int32 row_ptr[NB+1], col_idx[nnz])."""
+    import torch
+    nb, nnz, _ = plan_size(n, B, L)
+    if row_ptr is None:
+        row_ptr = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
+    if col_idx is None:
+        col_idx = torch.empty(max(nnz, 1), dtype=torch.int32, device="cuda")
+    for t in (row_ptr, col_idx):
+        if not (t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()):
+            raise ValueError("row_ptr / col_idx must be contiguous int32 CUDA tensors")
+    if row_ptr.numel() < nb + 1:
+        raise ValueError("row_ptr too small")
+    _check(load().bf1_plan(int(n), int(B), int(L), _ptr(row_ptr), _ptr(col_idx),
+                           col_idx.numel(), _stream(stream)), "bf1_plan")
+    return row_ptr, col_idx[:nnz]
+
+
+def _prep(q, k, v, out, lse, want_lse):
+    import torch
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not t.is_cuda or t.dtype != torch.bfloat16 or t.dim() != 4 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous 4-D bf16 CUDA tensor")
+    batch, Hq, n, d = q.shape
+    if k.shape != v.shape or k.shape[0] != batch or k.shape[2] != n or k.shape[3] != d:
+        raise ValueError("k and v must be [batch, Hkv, n, d] matching q")
+    Hkv = k.shape[1]
+    if out is None:
+        out = torch.empty_like(q)
+    elif out.shape != q.shape or out.dtype != torch.bfloat16 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous bf16 tensor shaped like q")
+    if lse is None and want_lse:
+        lse = torch.empty((batch, Hq, n), dtype=torch.float32, device=q.device)
+    if lse is not None and (lse.shape != (batch, Hq, n) or lse.dtype != torch.float32
+                            or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 tensor [batch, Hq, n]")
+    return out, lse, (batch, n, Hq, Hkv, d)
+
+
+def attn_fwd(q, k, v, B=64, L=2, out=None, lse=None, want_lse=True, stream=None):
+    """BF1 prefill forward; returns (O, LSE)."""
+    out, lse, (batch, n, Hq, Hkv, d) = _prep(q, k, v, out, lse, want_lse)
+    _check(load().bf1_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch, n, Hq,
+                               Hkv, d, int(B), int(L), _stream(stream)), "bf1_attn_fwd")
+    return out, lse
+
+
+def attn_fwd_csr(q, k, v, B, row_ptr, col_idx, out=None, lse=None, want_lse=True, stream=None):
+    """Forward over a caller-supplied block route (CSR, int32 CUDA tensors)."""
+    import torch
+    for t in (row_ptr, col_idx):
+        if not (t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()):
+            raise ValueError("row_ptr / col_idx must be contiguous int32 CUDA tensors")
+    out, lse, (batch, n, Hq, Hkv, d) = _prep(q, k, v, out, lse, want_lse)
+    nb = -(-n // int(B))
+    if row_ptr.numel() < nb + 1:
+        raise ValueError("row_ptr must have ceil(n/B)+1 entries")
+    _check(load().bf1_attn_fwd_csr(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch, n,
+                                   Hq, Hkv, d, int(B), _ptr(row_ptr), _ptr(col_idx),
+                                   col_idx.numel(), _stream(stream)), "bf1_attn_fwd_csr")
+    return out, lse
+
+
+def dense_causal_fwd(q, k, v, out=None, lse=None, want_lse=True, stream=None):
+    """In-house dense causal attention built from the same kernel."""
+    out, lse, (batch, n, Hq, Hkv, d) = _prep(q, k, v, out, lse, want_lse)
+    _check(load().bf1_dense_causal_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch,
+                                       n, Hq, Hkv, d, _stream(stream)), "bf1_dense_causal_fwd")
+    return out, lse
+
+
+def release_plans():
+    load().bf1_release_plans()

@@ -1,0 +1,193 @@
+// C-ABI shim of libbf1.so: argument validation, the plan cache, stream
+// handling and the mapping of HIP errors to status codes.  Every argument
+// check happens before any HIP call, so invalid calls touch no device.
+#include <hip/hip_runtime_api.h>
+
+#include <map>
+#include <mutex>
+#include <tuple>
+
+#include "../../include/bf1.h"
+#include "bf1_kernels.h"
+#include "bf1_route.h"
+
+namespace {
+
+constexpr int kVersion = 10000;  // 1.0.0
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Route sizes; false if the table would not fit int32 indices.
+bool route_sizes(int64_t n, int64_t B, int64_t L, int64_t* NB, int64_t* nnz) {
+    *NB = (n + B - 1) / B;
+    if (*NB >= 0x7fffffff) return false;
+    *nnz = bf1::route_row_start(*NB, L);
+    return *nnz >= 0 && *nnz < 0x7fffffff;
+}
+
+// ---- plan cache: (device, n, B, L) -> device CSR --------------------------
+struct Plan {
+    int32_t* row_ptr = nullptr;
+    int32_t* col_idx = nullptr;
+    int64_t nnz = 0;
+    hipEvent_t ready = nullptr;  // recorded after the planner kernel
+};
+
+std::mutex g_mu;
+std::map<std::tuple<int, int64_t, int32_t, int32_t>, Plan> g_plans;
+
+int status_of(hipError_t e) { return e == hipSuccess ? BF1_OK : BF1_ERR_HIP; }
+
+// Validation shared by the attention entry points.
+int check_attn(const void* Q, const void* K, const void* V, void* O, float* LSE, int32_t batch,
+               int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim) {
+    if (batch < 0 || n < 0 || Hq < 1 || Hkv < 1) return BF1_ERR_INVALID_ARG;
+    if (Hq % Hkv != 0) return BF1_ERR_INVALID_ARG;
+    if (n > 0x7fffffffLL - 256) return BF1_ERR_INVALID_ARG;
+    const int32_t G = Hq / Hkv;
+    if (head_dim != 64 && head_dim != 128) return BF1_ERR_UNSUPPORTED;
+    if (G != 1 && G != 2 && G != 4 && G != 8) return BF1_ERR_UNSUPPORTED;
+    if (batch == 0 || n == 0) return BF1_OK;
+    if (!Q || !K || !V || !O) return BF1_ERR_INVALID_ARG;
+    if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16))
+        return BF1_ERR_INVALID_ARG;
+    if (LSE && !aligned(LSE, 4)) return BF1_ERR_INVALID_ARG;
+    // element counts must fit comfortably in int64 byte offsets
+    const double elems = (double)batch * (double)Hq * (double)n * (double)head_dim;
+    if (elems > 4.0e18) return BF1_ERR_INVALID_ARG;
+    return BF1_OK;
+}
+
+int run_attn(const bf1::AttnArgs& a, hipStream_t s) { return status_of(bf1::launch_attention(a, s)); }
+
+}  // namespace
+
+extern "C" {
+
+int bf1_version(void) { return kVersion; }
+
+const char* bf1_status_string(int status) {
+    switch (status) {
+        case BF1_OK: return "BF1_OK";
+        case BF1_ERR_INVALID_ARG: return "BF1_ERR_INVALID_ARG: invalid argument";
+        case BF1_ERR_UNSUPPORTED: return "BF1_ERR_UNSUPPORTED: configuration not supported";
+        case BF1_ERR_BUFFER_TOO_SMALL: return "BF1_ERR_BUFFER_TOO_SMALL: route table capacity too small";
+        case BF1_ERR_HIP: return "BF1_ERR_HIP: HIP runtime or launch error";
+        case BF1_ERR_NOMEM: return "BF1_ERR_NOMEM: device allocation failed";
+        default: return "BF1: unknown status";
+    }
+}
+
+int bf1_plan_size(int64_t n, int32_t B, int32_t L, int32_t* num_blocks, int64_t* nnz,
+                  int64_t* pairs) {
+    if (n < 0 || B < 1 || L < 0) return BF1_ERR_INVALID_ARG;
+    int64_t NB, z;
+    if (!route_sizes(n, B, L, &NB, &z)) return BF1_ERR_INVALID_ARG;
+    if (num_blocks) *num_blocks = (int32_t)NB;
+    if (nnz) *nnz = z;
+    if (pairs) *pairs = bf1::route_selected_pairs(n, B, L);
+    return BF1_OK;
+}
+
+int bf1_plan(int64_t n, int32_t B, int32_t L, int32_t* row_ptr, int32_t* col_idx,
+             int64_t col_capacity, void* stream) {
+    if (n < 0 || B < 1 || L < 0 || col_capacity < 0) return BF1_ERR_INVALID_ARG;
+    int64_t NB, nnz;
+    if (!route_sizes(n, B, L, &NB, &nnz)) return BF1_ERR_INVALID_ARG;
+    if (!row_ptr) return BF1_ERR_INVALID_ARG;
+    if (nnz > 0 && !col_idx) return BF1_ERR_INVALID_ARG;
+    if (!aligned(row_ptr, 4) || (col_idx && !aligned(col_idx, 4))) return BF1_ERR_INVALID_ARG;
+    if (col_capacity < nnz) return BF1_ERR_BUFFER_TOO_SMALL;
+    return status_of(bf1::launch_plan((int32_t)NB, L, row_ptr, col_idx, (hipStream_t)stream));
+}
+
+int bf1_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE, int32_t batch,
+                 int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t B, int32_t L,
+                 void* stream) {
+    int st = check_attn(Q, K, V, O, LSE, batch, n, Hq, Hkv, head_dim);
+    if (st != BF1_OK) return st;
+    if (L < 0) return BF1_ERR_INVALID_ARG;
+    if (B != 64 && B != 128) return BF1_ERR_UNSUPPORTED;
+    if (batch == 0 || n == 0) return BF1_OK;
+    int64_t NB, nnz;
+    if (!route_sizes(n, B, L, &NB, &nnz)) return BF1_ERR_INVALID_ARG;
+    hipStream_t s = (hipStream_t)stream;
+
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return BF1_ERR_HIP;
+    Plan plan;
+    {
+        std::lock_guard<std::mutex> lock(g_mu);
+        auto key = std::make_tuple(dev, n, B, L);
+        auto it = g_plans.find(key);
+        if (it == g_plans.end()) {
+            Plan p;
+            p.nnz = nnz;
+            if (hipMalloc((void**)&p.row_ptr, sizeof(int32_t) * (NB + 1)) != hipSuccess)
+                return BF1_ERR_NOMEM;
+            if (hipMalloc((void**)&p.col_idx, sizeof(int32_t) * (nnz > 0 ? nnz : 1)) != hipSuccess) {
+                (void)hipFree(p.row_ptr);
+                return BF1_ERR_NOMEM;
+            }
+            if (hipEventCreateWithFlags(&p.ready, hipEventDisableTiming) != hipSuccess) {
+                (void)hipFree(p.row_ptr);
+                (void)hipFree(p.col_idx);
+                return BF1_ERR_HIP;
+            }
+            hipError_t e = bf1::launch_plan((int32_t)NB, L, p.row_ptr, p.col_idx, s);
+            if (e == hipSuccess) e = hipEventRecord(p.ready, s);
+            if (e != hipSuccess) {
+                (void)hipFree(p.row_ptr);
+                (void)hipFree(p.col_idx);
+                (void)hipEventDestroy(p.ready);
+                return BF1_ERR_HIP;
+            }
+            it = g_plans.emplace(key, p).first;
+        }
+        plan = it->second;
+    }
+    // The plan may have been built on another stream: order this one after it.
+    if (hipStreamWaitEvent(s, plan.ready, 0) != hipSuccess) return BF1_ERR_HIP;
+
+    bf1::AttnArgs a{Q, K, V, O, LSE, plan.row_ptr, plan.col_idx, plan.nnz,
+                    batch, n, Hq, Hkv, head_dim, B, false};
+    return run_attn(a, s);
+}
+
+int bf1_attn_fwd_csr(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                     int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                     int32_t B, const int32_t* row_ptr, const int32_t* col_idx, int64_t nnz,
+                     void* stream) {
+    int st = check_attn(Q, K, V, O, LSE, batch, n, Hq, Hkv, head_dim);
+    if (st != BF1_OK) return st;
+    if (B != 64 && B != 128) return BF1_ERR_UNSUPPORTED;
+    if (nnz < 0 || nnz >= 0x7fffffff) return BF1_ERR_INVALID_ARG;
+    if (batch == 0 || n == 0) return BF1_OK;
+    if (!row_ptr || (nnz > 0 && !col_idx)) return BF1_ERR_INVALID_ARG;
+    if (!aligned(row_ptr, 4) || (col_idx && !aligned(col_idx, 4))) return BF1_ERR_INVALID_ARG;
+    bf1::AttnArgs a{Q, K, V, O, LSE, row_ptr, col_idx, nnz, batch, n, Hq, Hkv, head_dim, B, false};
+    return run_attn(a, (hipStream_t)stream);
+}
+
+int bf1_dense_causal_fwd(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                         int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                         void* stream) {
+    int st = check_attn(Q, K, V, O, LSE, batch, n, Hq, Hkv, head_dim);
+    if (st != BF1_OK) return st;
+    if (batch == 0 || n == 0) return BF1_OK;
+    bf1::AttnArgs a{Q, K, V, O, LSE, nullptr, nullptr, 0, batch, n, Hq, Hkv, head_dim, 64, true};
+    return run_attn(a, (hipStream_t)stream);
+}
+
+void bf1_release_plans(void) {
+    std::lock_guard<std::mutex> lock(g_mu);
+    for (auto& kv : g_plans) {
+        (void)hipEventSynchronize(kv.second.ready);
+        (void)hipFree(kv.second.row_ptr);
+        (void)hipFree(kv.second.col_idx);
+        (void)hipEventDestroy(kv.second.ready);
+    }
+    g_plans.clear();
+}
+
+}  // extern "C"

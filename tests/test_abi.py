@@ -1,0 +1,105 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, computes route sizes in closed form (host code) that agree
+with the oracle's enumeration, and rejects bad arguments before any device
+call."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_20427_amd as bf1
+from oracle import bf1_oracle as orc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bf1.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(bf1_[a-z_0-9]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(bf1.lib_path()):
+        pytest.fail("libbf1.so is not built (run __graft_entry__.build())")
+    return bf1.load()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for want in ["bf1_plan", "bf1_plan_size", "bf1_attn_fwd", "bf1_attn_fwd_csr",
+                 "bf1_dense_causal_fwd", "bf1_release_plans", "bf1_status_string", "bf1_version"]:
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for st in range(-5, 1):
+        assert bf1.status_string(st).startswith("BF1")
+    assert "unknown" in bf1.status_string(42)
+    assert bf1.version() >= 10000
+
+
+@pytest.mark.parametrize("n,B,L", [(512, 64, 1), (4096, 64, 2), (32768, 64, 2), (30001, 64, 2),
+                                   (65536, 128, 2), (1, 64, 2), (0, 64, 2), (777, 5, 0),
+                                   (100000, 64, 7)])
+def test_plan_size_matches_oracle(lib, n, B, L):
+    nb, nnz, pairs = bf1.plan_size(n, B, L)
+    rp, ci = orc.csr(n, B, L)
+    assert nb == len(rp) - 1 and nnz == len(ci)
+    assert pairs == orc.selected_pairs(n, B, L)
+
+
+def test_selected_flops_headline(lib):
+    # 32K tokens, Qwen3-0.6B geometry: 4 * 128 * pairs * 16 q-heads.
+    f = bf1.selected_flops(1, 32768, 16, 128, 64, 2)
+    assert f == 4 * 128 * orc.selected_pairs(32768, 64, 2) * 16
+    assert abs(f / 1e9 - 163.04) < 0.01
+
+
+def test_invalid_arguments_rejected_without_device(lib):
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: checks come first
+    st = lib.bf1_attn_fwd(fake, fake, fake, fake, None, 1, 128, 2, 1, 96, 64, 2, None)
+    assert st == bf1.BF1_ERR_UNSUPPORTED
+    st = lib.bf1_attn_fwd(fake, fake, fake, fake, None, 1, 128, 2, 1, 128, 48, 2, None)
+    assert st == bf1.BF1_ERR_UNSUPPORTED
+    st = lib.bf1_attn_fwd(fake, fake, fake, fake, None, 1, 128, 3, 2, 128, 64, 2, None)
+    assert st == bf1.BF1_ERR_INVALID_ARG
+    st = lib.bf1_attn_fwd(fake, fake, fake, fake, None, 1, 128, 6, 2, 128, 64, 2, None)
+    assert st == bf1.BF1_ERR_UNSUPPORTED     # group of 3
+    st = lib.bf1_attn_fwd(None, fake, fake, fake, None, 1, 128, 2, 1, 128, 64, 2, None)
+    assert st == bf1.BF1_ERR_INVALID_ARG
+    st = lib.bf1_attn_fwd(ctypes.c_void_p((1 << 20) + 8), fake, fake, fake, None, 1, 128, 2, 1,
+                          128, 64, 2, None)
+    assert st == bf1.BF1_ERR_INVALID_ARG     # misaligned
+    st = lib.bf1_attn_fwd(fake, fake, fake, fake, None, 1, -5, 2, 1, 128, 64, 2, None)
+    assert st == bf1.BF1_ERR_INVALID_ARG
+    st = lib.bf1_attn_fwd(fake, fake, fake, fake, None, 1, 128, 2, 1, 128, 64, -1, None)
+    assert st == bf1.BF1_ERR_INVALID_ARG
+    st = lib.bf1_dense_causal_fwd(fake, fake, fake, fake, None, 1, 128, 2, 1, 80, None)
+    assert st == bf1.BF1_ERR_UNSUPPORTED
+    st = lib.bf1_attn_fwd_csr(fake, fake, fake, fake, None, 1, 128, 2, 1, 128, 64, None, fake, 4,
+                              None)
+    assert st == bf1.BF1_ERR_INVALID_ARG
+    # plan: capacity below the route size is reported before any launch
+    nb, nnz, _ = bf1.plan_size(4096, 64, 2)
+    st = lib.bf1_plan(4096, 64, 2, fake, fake, nnz - 1, None)
+    assert st == bf1.BF1_ERR_BUFFER_TOO_SMALL
+    st = lib.bf1_plan(4096, 0, 2, fake, fake, nnz, None)
+    assert st == bf1.BF1_ERR_INVALID_ARG
+
+
+def test_empty_problems_are_noops(lib):
+    # n == 0 / batch == 0 return before touching the device.
+    st = lib.bf1_attn_fwd(None, None, None, None, None, 0, 128, 2, 1, 128, 64, 2, None)
+    assert st == bf1.BF1_OK
+    st = lib.bf1_dense_causal_fwd(None, None, None, None, None, 1, 0, 2, 1, 128, None)
+    assert st == bf1.BF1_OK

@@ -1,0 +1,389 @@
+"""GPU parity of the HIP path against the fp64 CPU oracle.
+
+Bars (fixed before any kernel was written):
+  * route tables: bit-exact against the oracle's enumeration of Eq. 1;
+  * O: max-abs <= 2e-2 and mean-abs <= 2e-3 against fp64 on the same bf16
+    inputs; LSE (natural log): max-abs <= 1e-3;
+  * future-token isolation, prefix consistency, determinism: bitwise.
+"""
+
+import math
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_20427_amd as bf1
+from oracle import bf1_oracle as orc
+from paper_2608_20427_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+O_MAX, O_MEAN, LSE_MAX = 2e-2, 2e-3, 1e-3
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    bf1.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def sample_blocks(NB, count, seed):
+    if NB <= count:
+        return list(range(NB))
+    rng = np.random.default_rng(seed)
+    mid = rng.choice(np.arange(1, NB - 1), size=count - 2, replace=False)
+    return sorted({0, NB - 1, *mid.tolist()})
+
+
+def rows_of(blocks, b, n):
+    return np.concatenate([np.arange(j * b, min((j + 1) * b, n)) for j in blocks])
+
+
+def compare(o_gpu, lse_gpu, o_ref, lse_ref, rows=None, tag=""):
+    o = o_gpu.float().cpu().double().numpy()
+    l = lse_gpu.cpu().double().numpy()
+    if rows is not None:
+        o, l = o[:, :, rows], l[:, :, rows]
+        o_ref, lse_ref = o_ref[:, :, rows], lse_ref[:, :, rows]
+    assert np.isfinite(o).all() and np.isfinite(l).all(), tag
+    err = np.abs(o - o_ref)
+    lerr = np.abs(l - lse_ref)
+    say(f"[{tag}] O max {err.max():.3e} mean {err.mean():.3e} | LSE max {lerr.max():.3e}")
+    assert err.max() <= O_MAX, tag
+    assert err.mean() <= O_MEAN, tag
+    assert lerr.max() <= LSE_MAX, tag
+
+
+def run_bf1(w):
+    q, k, v = synth.make_qkv(w, device="cuda")
+    o, lse = bf1.attn_fwd(q, k, v, B=w.b, L=w.L)
+    torch.cuda.synchronize()
+    return (q, k, v), o, lse
+
+
+# ---------------------------------------------------------------------------
+# Route planner: bit-exact
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n,B,L", [(512, 64, 1), (4096, 64, 2), (32768, 64, 2), (30001, 64, 2),
+                                   (65536, 64, 2), (65536, 128, 2), (1, 64, 2), (257, 64, 2),
+                                   (100000, 16, 3), (5000, 7, 0), (70000, 64, 9)])
+def test_plan_bit_exact(n, B, L):
+    say(f"plan n={n} B={B} L={L}")
+    rp, ci = bf1.plan(n, B, L)
+    torch.cuda.synchronize()
+    rp_ref, ci_ref = orc.csr(n, B, L)
+    assert np.array_equal(rp.cpu().numpy(), rp_ref)
+    assert np.array_equal(ci.cpu().numpy(), ci_ref)
+    nb, nnz, pairs = bf1.plan_size(n, B, L)
+    assert nb == len(rp_ref) - 1 and nnz == len(ci_ref)
+    assert pairs == orc.selected_pairs(n, B, L)
+
+
+def test_plan_random_configs():
+    rng = np.random.default_rng(123)
+    for _ in range(40):
+        n = int(rng.integers(0, 20000))
+        B = int(rng.choice([16, 32, 64, 128, 3]))
+        L = int(rng.integers(0, 6))
+        rp, ci = bf1.plan(n, B, L)
+        torch.cuda.synchronize()
+        rp_ref, ci_ref = orc.csr(n, B, L)
+        assert np.array_equal(rp.cpu().numpy(), rp_ref), (n, B, L)
+        assert np.array_equal(ci.cpu().numpy()[: len(ci_ref)], ci_ref), (n, B, L)
+
+
+def test_plan_buffer_too_small():
+    nb, nnz, _ = bf1.plan_size(4096, 64, 2)
+    rp = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
+    ci = torch.empty(nnz - 1, dtype=torch.int32, device="cuda")
+    with pytest.raises(bf1.BF1Error) as e:
+        bf1.plan(4096, 64, 2, rp, ci)
+    assert e.value.status == bf1.BF1_ERR_BUFFER_TOO_SMALL
+
+
+# ---------------------------------------------------------------------------
+# Attention parity: small shapes, full oracle
+# ---------------------------------------------------------------------------
+
+SMALL = [
+    # batch, n, Hq, Hkv, d, B, L
+    (1, 512, 2, 1, 64, 64, 1),      # the tiny workload
+    (1, 257, 2, 1, 128, 64, 2),     # partial block of one token
+    (2, 1000, 4, 2, 128, 64, 2),    # ragged tail (1000 = 15*64 + 40)
+    (1, 777, 4, 1, 64, 64, 3),      # G = 4
+    (1, 640, 8, 1, 128, 64, 2),     # G = 8
+    (1, 700, 3, 3, 128, 64, 2),     # G = 1 (MHA)
+    (1, 900, 2, 2, 64, 128, 2),     # B = 128, G = 1
+    (1, 1500, 4, 2, 128, 128, 2),   # B = 128, ragged
+    (1, 2048, 16, 8, 128, 64, 2),   # Qwen geometry, short
+    (1, 1, 2, 1, 128, 64, 2),       # a single token
+    (1, 5, 2, 1, 64, 64, 2),        # n < B
+    (1, 65, 2, 1, 128, 64, 2),      # n = B + 1
+    (1, 130, 2, 1, 128, 128, 0),    # L = 0
+]
+
+
+@pytest.mark.parametrize("cfg", SMALL, ids=lambda c: "x".join(map(str, c)))
+def test_attn_small_full_oracle(cfg):
+    batch, n, Hq, Hkv, d, B, L = cfg
+    say(f"attn small {cfg}")
+    w = synth.Workload("small", batch, n, Hq, Hkv, d, B, L, seed=100 + n + d)
+    (q, k, v), o, lse = run_bf1(w)
+    o_ref, l_ref = orc.attn_gathered_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), B, L)
+    compare(o, lse, o_ref, l_ref, tag=str(cfg))
+
+
+def test_tiny_workload_full_mask_oracle():
+    w = synth.WORKLOADS["tiny_n512"]
+    (q, k, v), o, lse = run_bf1(w)
+    o_ref, l_ref = orc.attn_full_mask_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), w.b, w.L)
+    compare(o, lse, o_ref, l_ref, tag="tiny full mask")
+
+
+def test_qwen_4096_full_oracle():
+    w = synth.WORKLOADS["qwen_n4096"]
+    say("qwen n=4096 full")
+    (q, k, v), o, lse = run_bf1(w)
+    o_ref, l_ref = orc.attn_gathered_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), w.b, w.L)
+    compare(o, lse, o_ref, l_ref, tag="qwen_n4096")
+
+
+@pytest.mark.parametrize("name", ["qwen_n32768", "qwen_n30001_b2_peaked"])
+def test_full_size_sampled_blocks(name):
+    # Full-size workloads in the launch configuration the benchmark times;
+    # the oracle checks a seeded sample of query blocks (first, last, random).
+    w = synth.WORKLOADS[name]
+    say(f"full size {name}")
+    (q, k, v), o, lse = run_bf1(w)
+    NB = orc.num_blocks(w.n, w.b)
+    blocks = sample_blocks(NB, 20, seed=w.seed)
+    o_ref, l_ref = orc.attn_gathered_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), w.b,
+                                          w.L, blocks=blocks)
+    compare(o, lse, o_ref, l_ref, rows=rows_of(blocks, w.b, w.n), tag=name)
+    # every output row written and finite
+    assert torch.isfinite(o).all() and torch.isfinite(lse).all()
+
+
+def test_sweep_64k_sampled():
+    w = synth.sweep(64)[-1]
+    assert w.n == 65536
+    (q, k, v), o, lse = run_bf1(w)
+    blocks = sample_blocks(orc.num_blocks(w.n, w.b), 8, seed=1)
+    o_ref, l_ref = orc.attn_gathered_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), w.b,
+                                          w.L, blocks=blocks)
+    compare(o, lse, o_ref, l_ref, rows=rows_of(blocks, w.b, w.n), tag="n65536")
+
+
+def test_b128_32k_sampled():
+    w = synth.sweep(128)[5]
+    assert w.n == 32768 and w.b == 128
+    (q, k, v), o, lse = run_bf1(w)
+    blocks = sample_blocks(orc.num_blocks(w.n, w.b), 8, seed=2)
+    o_ref, l_ref = orc.attn_gathered_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), w.b,
+                                          w.L, blocks=blocks)
+    compare(o, lse, o_ref, l_ref, rows=rows_of(blocks, w.b, w.n), tag="n32768 b128")
+
+
+# ---------------------------------------------------------------------------
+# Dense causal comparator
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("cfg", [(1, 512, 2, 1, 64), (1, 1000, 4, 2, 128), (2, 333, 8, 1, 128),
+                                 (1, 2048, 16, 8, 128)])
+def test_dense_small(cfg):
+    batch, n, Hq, Hkv, d = cfg
+    w = synth.Workload("dense", batch, n, Hq, Hkv, d, 64, 2, seed=7 + n)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    o, lse = bf1.dense_causal_fwd(q, k, v)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(min(n, 70)), np.arange(max(0, n - 70), n),
+                                     np.random.default_rng(1).integers(0, n, 60)]))
+    o_ref, l_ref = orc.dense_causal_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), rows=rows)
+    compare(o, lse, o_ref, l_ref, rows=rows, tag=f"dense {cfg}")
+
+
+def test_dense_32k_sampled_rows():
+    w = synth.WORKLOADS["qwen_n32768"]
+    q, k, v = synth.make_qkv(w, device="cuda")
+    o, lse = bf1.dense_causal_fwd(q, k, v)
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 63, 64, 4095, 16384, 32766, 32767])
+    o_ref, l_ref = orc.dense_causal_fp64(synth.to_f64(q)[:, :4], synth.to_f64(k)[:, :2],
+                                         synth.to_f64(v)[:, :2], rows=rows)
+    compare(o[:, :4], lse[:, :4], o_ref, l_ref, rows=rows, tag="dense 32k")
+
+
+@pytest.mark.parametrize("n,L", [(1000, 14), (256, 2), (640, 100)])
+def test_bf1_covering_route_equals_dense_kernel(n, L):
+    # When the route covers every block, BF1 is dense causal attention; with
+    # B = 64 both kernels visit the same tiles in the same order.
+    w = synth.Workload("cover", 1, n, 4, 2, 128, 64, L, seed=3)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    o1, l1 = bf1.attn_fwd(q, k, v, B=64, L=L)
+    o2, l2 = bf1.dense_causal_fwd(q, k, v)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+# ---------------------------------------------------------------------------
+# Invariances and hygiene
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("t0", [1, 64, 100, 4095, 2500])
+def test_future_token_isolation(t0):
+    w = synth.Workload("iso", 1, 4096, 16, 8, 128, 64, 2, seed=9)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    o, l = bf1.attn_fwd(q, k, v)
+    q2, k2, v2 = q.clone(), k.clone(), v.clone()
+    g = torch.Generator(device="cpu").manual_seed(t0)
+    for x in (q2, k2, v2):
+        x[:, :, t0:] = (torch.randn(x[:, :, t0:].shape, generator=g) * 4).to(x.dtype).cuda()
+    o2, l2 = bf1.attn_fwd(q2, k2, v2)
+    torch.cuda.synchronize()
+    assert torch.equal(o[:, :, :t0], o2[:, :, :t0])
+    assert torch.equal(l[:, :, :t0], l2[:, :, :t0])
+    assert not torch.equal(o[:, :, t0:], o2[:, :, t0:])
+
+
+def test_prefix_consistency():
+    # The route does not depend on n: rows < n' agree when run at n' < n.
+    w = synth.Workload("pre", 1, 3000, 4, 2, 128, 64, 2, seed=12)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    o, l = bf1.attn_fwd(q, k, v)
+    for n2 in (1, 64, 1000, 2017):
+        o2, l2 = bf1.attn_fwd(q[:, :, :n2].contiguous(), k[:, :, :n2].contiguous(),
+                              v[:, :, :n2].contiguous())
+        torch.cuda.synchronize()
+        assert torch.equal(o[:, :, :n2], o2) and torch.equal(l[:, :, :n2], l2), n2
+
+
+def test_outputs_fully_written_and_nothing_else():
+    w = synth.Workload("sent", 2, 1000, 4, 2, 128, 64, 2, seed=13)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    numel = q.numel()
+    obuf = torch.full((numel + 4096,), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lbuf = torch.full((2 * 4 * 1000 + 1024,), float("nan"), dtype=torch.float32, device="cuda")
+    o = obuf[:numel].view(q.shape)
+    l = lbuf[: 2 * 4 * 1000].view(2, 4, 1000)
+    bf1.attn_fwd(q, k, v, out=o, lse=l)
+    torch.cuda.synchronize()
+    assert torch.isfinite(o).all() and torch.isfinite(l).all()
+    assert torch.isnan(obuf[numel:]).all() and torch.isnan(lbuf[2 * 4 * 1000:]).all()
+
+
+def test_deterministic():
+    w = synth.WORKLOADS["qwen_n4096"]
+    q, k, v = synth.make_qkv(w, device="cuda")
+    o1, l1 = bf1.attn_fwd(q, k, v)
+    o2, l2 = bf1.attn_fwd(q, k, v)
+    d1, e1 = bf1.dense_causal_fwd(q, k, v)
+    d2, e2 = bf1.dense_causal_fwd(q, k, v)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    assert torch.equal(d1, d2) and torch.equal(e1, e2)
+
+
+def test_lse_optional():
+    w = synth.Workload("nolse", 1, 700, 4, 2, 128, 64, 2, seed=14)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    o1, _ = bf1.attn_fwd(q, k, v)
+    o2, l2 = bf1.attn_fwd(q, k, v, want_lse=False)
+    torch.cuda.synchronize()
+    assert l2 is None and torch.equal(o1, o2)
+
+
+def test_empty_inputs_are_noops():
+    for n, batch in ((0, 1), (100, 0)):
+        q = torch.empty((batch, 2, n, 128), dtype=torch.bfloat16, device="cuda")
+        k = torch.empty((batch, 1, n, 128), dtype=torch.bfloat16, device="cuda")
+        o, l = bf1.attn_fwd(q, k, k)
+        o, l = bf1.dense_causal_fwd(q, k, k)
+    rp, ci = bf1.plan(0, 64, 2)
+    torch.cuda.synchronize()
+    assert rp.cpu().tolist() == [0] and ci.numel() == 0
+
+
+def test_unsupported_configs_raise():
+    q = torch.zeros((1, 2, 64, 96), dtype=torch.bfloat16, device="cuda")
+    k = torch.zeros((1, 1, 64, 96), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(bf1.BF1Error) as e:
+        bf1.attn_fwd(q, k, k)
+    assert e.value.status == bf1.BF1_ERR_UNSUPPORTED
+    q = torch.zeros((1, 2, 64, 128), dtype=torch.bfloat16, device="cuda")
+    k = torch.zeros((1, 1, 64, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(bf1.BF1Error) as e:
+        bf1.attn_fwd(q, k, k, B=32)
+    assert e.value.status == bf1.BF1_ERR_UNSUPPORTED
+    q3 = torch.zeros((1, 3, 64, 128), dtype=torch.bfloat16, device="cuda")
+    k2 = torch.zeros((1, 2, 64, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(bf1.BF1Error) as e:
+        bf1.attn_fwd(q3, k2, k2)
+    assert e.value.status == bf1.BF1_ERR_INVALID_ARG
+
+
+def test_plan_cache_across_streams():
+    w = synth.Workload("strm", 1, 2000, 4, 2, 128, 64, 2, seed=15)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    bf1.release_plans()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        o1, l1 = bf1.attn_fwd(q, k, v)
+    s.synchronize()
+    o2, l2 = bf1.attn_fwd(q, k, v)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+# ---------------------------------------------------------------------------
+# Caller-supplied routes through the CSR entry point
+# ---------------------------------------------------------------------------
+
+def sliding_csr(NB, width):
+    rows = [list(range(max(0, j - width), j + 1)) for j in range(NB)]
+    rp = np.zeros(NB + 1, dtype=np.int32)
+    for j, r in enumerate(rows):
+        rp[j + 1] = rp[j] + len(r)
+    return rp, np.array([i for r in rows for i in r], dtype=np.int32)
+
+
+@pytest.mark.parametrize("B", [64, 128])
+def test_csr_sliding_route(B):
+    n = 3000
+    NB = -(-n // B)
+    rp, ci = sliding_csr(NB, 5)
+    w = synth.Workload("slide", 1, n, 4, 2, 128, B, 2, seed=16)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    o, l = bf1.attn_fwd_csr(q, k, v, B, torch.from_numpy(rp).cuda(), torch.from_numpy(ci).cuda())
+    torch.cuda.synchronize()
+    o_ref, l_ref = orc.attn_csr_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), B, rp, ci)
+    compare(o, l, o_ref, l_ref, tag=f"sliding B={B}")
+
+
+def test_csr_out_of_range_entries_are_ignored():
+    # Entries beyond the causal range (> j) or negative are skipped, never read.
+    n, B = 640, 64
+    NB = n // B
+    rp_ref, ci_ref = orc.csr(n, B, 2)
+    rows = [list(ci_ref[rp_ref[j]:rp_ref[j + 1]]) + [j + 3, -7, 10**6] for j in range(NB)]
+    rp = np.zeros(NB + 1, dtype=np.int32)
+    for j, r in enumerate(rows):
+        rp[j + 1] = rp[j] + len(r)
+    ci = np.array([i for r in rows for i in r], dtype=np.int32)
+    w = synth.Workload("oor", 1, n, 2, 1, 128, B, 2, seed=17)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    o, l = bf1.attn_fwd_csr(q, k, v, B, torch.from_numpy(rp).cuda(), torch.from_numpy(ci).cuda())
+    o2, l2 = bf1.attn_fwd(q, k, v, B=B, L=2)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o2) and torch.equal(l, l2)
