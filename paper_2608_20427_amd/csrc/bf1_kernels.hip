@@ -46,6 +46,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int KT = 64;  // keys per LDS tile
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
+constexpr float RESCALE_LOG2 = 8.0f;  // lazy-rescale threshold (log2 units)
 
 // ---------------------------------------------------------------------------
 // Route planner
@@ -114,7 +115,7 @@ struct TileSmem {
 // ---------------------------------------------------------------------------
 
 template <int D, int G, int BW, int NW, bool DENSE>
-__global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(
+__global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     __bf16* __restrict__ O, float* __restrict__ LSE, const int32_t* __restrict__ row_ptr,
     const int32_t* __restrict__ col_idx, int64_t nnz, int32_t n, int32_t NB, int32_t batch_hkv,
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
     const int col = lane & 31;   // query column owned by this lane
     const int half = lane >> 5;  // lane half: selects k-range / row group
 
@@ -184,18 +185,14 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(
         pos_end = (int32_t)e1;
     }
     // Advance (p, u) to the next tile that exists: a valid block i in [0, j]
-    // whose sub-tile u starts before n.
+    // whose sub-tile u starts before n.  All quantities fit in 32 bits
+    // (i * BW < n + BW < 2^31).
     auto seek = [&](int32_t& p, int& u, int32_t& i) -> bool {
-        while (p < pos_end) {
+        for (; p < pos_end; ++p, u = 0) {
             i = DENSE ? p : col_idx[p];
-            if (i >= 0 && i <= j) {
-                while (u < NSUB) {
-                    if ((int64_t)i * BW + u * KT < n) return true;
-                    ++u;
-                }
-            }
-            ++p;
-            u = 0;
+            if (i < 0 || i > j) continue;
+            for (; u < NSUB; ++u)
+                if (i * BW + u * KT < n) return true;
         }
         return false;
     };
@@ -207,28 +204,31 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(
     u32x4 kreg[KLD];
     u32x4 vreg[VLD][4];
 
+    // Keys at or past n occur only in the self block of the last query block,
+    // where every query that exists sees them with probability exactly 0.
+    // Their rows are therefore loaded from a clamped, valid row of the same
+    // tile (finite data, 0 * finite = 0) instead of being zeroed, so the
+    // loaded registers are never touched before they are stored to LDS and
+    // the loads stay in flight across the compute of the current tile.
     auto load_tile = [&](int32_t i, int u) {
         const int32_t key0 = i * BW + u * KT;
+        const __bf16* kb = Kh + (int64_t)key0 * D;
+        const __bf16* vb = Vh + (int64_t)key0 * D;
+        const int32_t last = n - key0 - 1;  // last valid row of the tile (>= 0)
 #pragma unroll
         for (int it = 0; it < KLD; ++it) {
             const int idx = tid + it * NT;
-            const int kr = idx / DCH, c = idx % DCH;
-            u32x4 w = {0u, 0u, 0u, 0u};
-            if (key0 + kr < n)
-                w = *reinterpret_cast<const u32x4*>(Kh + (int64_t)(key0 + kr) * D + c * 8);
-            kreg[it] = w;
+            const int kr = min(idx / DCH, last), c = idx % DCH;
+            kreg[it] = *reinterpret_cast<const u32x4*>(kb + kr * D + c * 8);
         }
 #pragma unroll
         for (int it = 0; it < VLD; ++it) {
-            const int job = tid + it * NT;
+            const int job = (VJOBS % NT == 0) ? tid + it * NT : (tid % VJOBS);
             const int kg = job & 15, dc = job >> 4;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const int kr = 4 * kg + q;
-                u32x4 w = {0u, 0u, 0u, 0u};
-                if (job < VJOBS && key0 + kr < n)
-                    w = *reinterpret_cast<const u32x4*>(Vh + (int64_t)(key0 + kr) * D + dc * 8);
-                vreg[it][q] = w;
+                const int kr = min(4 * kg + q, last);
+                vreg[it][q] = *reinterpret_cast<const u32x4*>(vb + kr * D + dc * 8);
             }
         }
     };
@@ -243,8 +243,7 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(
         u32x2* vt = reinterpret_cast<u32x2*>(&sm.v[buf][0]);
 #pragma unroll
         for (int it = 0; it < VLD; ++it) {
-            const int job = tid + it * NT;
-            if (job >= VJOBS) continue;
+            const int job = (VJOBS % NT == 0) ? tid + it * NT : (tid % VJOBS);
             const int kg = job & 15, dc = job >> 4;
             const int lchunk = 2 * (kg >> 2) + (kg & 1);  // logical 16-B chunk of the 4 keys
             const int hsel = (kg >> 1) & 1;                // which 8-B half of it
@@ -268,7 +267,7 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(
     for (int t = 0; t < DT; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
-    float m_run = -INFINITY;  // running max, log2 units
+    float m_run = -1e30f;     // running max, log2 units (finite: masked scores give 0)
     float l_run = 0.f;        // this lane's partial row sum (its 32 keys of each tile)
 
     auto compute_tile = [&](int buf, int32_t i, int u) {
@@ -300,31 +299,40 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(
                     if (kp > qin) s[kt][r] = -INFINITY;
                 }
         }
-        // online softmax (log2 domain, c_log2 = scale * log2 e)
+        // Online softmax in the log2 domain (c_log2 = scale * log2 e).  A row's
+        // running max m_run only moves when a score exceeds it by more than
+        // 2^RESCALE_LOG2; otherwise the stale max is kept for numerator and
+        // denominator alike, which is exact and keeps every p <= 2^RESCALE_LOG2.
+        // The decision is per row (per lane), so a row's arithmetic never
+        // depends on other rows' data; the wave only skips the rescale work
+        // when no row needs it (alpha = 1 exactly for the others).
         float mx = -INFINITY;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
             for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx * c_log2);
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-        m_run = m_new;
+        const float m_cand = mx * c_log2;
+        const bool need = m_cand > m_run + RESCALE_LOG2;
+        if (__any(need)) {
+            const float alpha = need ? __builtin_amdgcn_exp2f(m_run - m_cand) : 1.0f;
+            m_run = need ? m_cand : m_run;
+            l_run *= alpha;
+#pragma unroll
+            for (int t = 0; t < DT; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[t][r] *= alpha;
+        }
         float ls = 0.f;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const float p = __builtin_amdgcn_exp2f(fmaf(s[kt][r], c_log2, -m_use));
+                const float p = __builtin_amdgcn_exp2f(fmaf(s[kt][r], c_log2, -m_run));
                 s[kt][r] = p;
                 ls += p;
             }
-        l_run = fmaf(l_run, alpha, ls);
-#pragma unroll
-        for (int t = 0; t < DT; ++t)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[t][r] *= alpha;
+        l_run += ls;
         // O^T += V^T P^T
         bf16x8 pb[4];
 #pragma unroll
@@ -349,14 +357,25 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(
     // ---- software pipeline: global loads of tile k+1 overlap compute of k ---
     int32_t cur_p = pos, cur_i = 0;
     int cur_u = 0;
-    bool have = seek(cur_p, cur_u, cur_i);
-    if (have) {
-        load_tile(cur_i, cur_u);
-        store_tile(0);
+    if (!seek(cur_p, cur_u, cur_i)) {
+        // A row with no usable key block (possible only for a caller route
+        // table): O = 0, LSE = -inf.
+        if (qvalid) {
+            __bf16* Orow = O + (((int64_t)beta * Hq + head) * (int64_t)n + qpos) * D;
+#pragma unroll
+            for (int c = 0; c < D / 2; c += 8)
+                *reinterpret_cast<u32x4*>(Orow + half * (D / 2) + c) = u32x4{0u, 0u, 0u, 0u};
+            if (LSE != nullptr && half == 0)
+                LSE[((int64_t)beta * Hq + head) * (int64_t)n + qpos] = -INFINITY;
+        }
+        return;
     }
+    load_tile(cur_i, cur_u);
+    store_tile(0);
     __syncthreads();
     int buf = 0;
-    while (have) {
+    bool have = true;
+    do {
         int32_t nxt_p = cur_p, nxt_i = 0;
         int nxt_u = cur_u + 1;
         const bool have_n = seek(nxt_p, nxt_u, nxt_i);
@@ -369,7 +388,7 @@ __global__ __launch_bounds__(NW * 64) void attn_fwd_kernel(
         cur_u = nxt_u;
         cur_i = nxt_i;
         have = have_n;
-    }
+    } while (have);
 
     // ---- epilogue: O = acc / l, LSE = (m + log2 l) ln 2 ---------------------
     const float l_tot = l_run + __shfl_xor(l_run, 32);
