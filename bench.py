@@ -56,6 +56,12 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time bound of the CPU oracle sample")
+    ap.add_argument("--calib-copy-mb", type=int, default=0,
+                    help="after timing, run one plain device copy of this many MiB (the "
+                         "reference for scaling HBM byte counters)")
+    ap.add_argument("--spinup-ms", type=float, default=200.0,
+                    help="untimed attention launches before the warmup steps so the GPU "
+                         "clocks have ramped up")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "bf1_fwd_traffic.json"))
     return ap.parse_args()
 
@@ -184,6 +190,13 @@ def main():
     def attn():
         bf1.attn_fwd_csr(q, k, v, w.b, rp, ci, out=o, lse=lse)
 
+    # clock spin-up (untimed, on a valid route table), then the W warmup steps
+    plan()
+    torch.cuda.synchronize()
+    t_spin = time.perf_counter()
+    while (time.perf_counter() - t_spin) * 1e3 < args.spinup_ms:
+        attn()
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         plan()
         attn()
@@ -240,6 +253,16 @@ def main():
                      "kernel": "attn_fwd_kernel<128,2,64,4,false>",
                      "kernel_ms": attn_ms},
     }
+
+    if args.calib_copy_mb > 0:
+        src = torch.empty(args.calib_copy_mb << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {args.calib_copy_mb} MiB done")
+        del src, dst
 
     if not args.no_dense:
         point = run_point(torch, bf1, w, q, k, v, args.warmup, args.reps)

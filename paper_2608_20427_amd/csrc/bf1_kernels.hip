@@ -29,6 +29,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "bf1_kernels.h"
 #include "bf1_route.h"
 
@@ -42,11 +44,13 @@ typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int KT = 64;  // keys per LDS tile
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 constexpr float RESCALE_LOG2 = 8.0f;  // lazy-rescale threshold (log2 units)
+constexpr int VMCNT0 = 0x0F70;        // s_waitcnt vmcnt(0) (expcnt, lgkmcnt unconstrained)
 
 // ---------------------------------------------------------------------------
 // Route planner
@@ -87,28 +91,74 @@ __global__ void bf1_plan_kernel(int32_t NB, int32_t L, int32_t* __restrict__ row
 }
 
 // ---------------------------------------------------------------------------
-// LDS tile layouts
+// LDS tile layouts (both tiles keep the natural [key][d] row order)
 // ---------------------------------------------------------------------------
-// K tile : KT rows (keys) x D bf16, stored as 16-byte chunks; chunk c of key
-//          row k sits at physical chunk c ^ kswz(k) so that the 16 lanes of
-//          one LDS cycle (consecutive keys, same logical chunk) hit 16
-//          distinct 4-bank groups.
-// V^T tile: D rows x KT key slots.  Inside each group of 16 keys, key
-//          16g + 8a + 4h + c (a,h in {0,1}, c in 0..3) is stored at slot
-//          16g + 8h + 4a + c, so the 8 keys that lane half h feeds to one PV
-//          MFMA k-step are one contiguous 16-byte chunk.  Chunks are swizzled
-//          by vswz(d) for the same reason as K.
+// K tile: KT rows x D bf16 in 16-byte chunks; logical chunk c of key row k
+//   sits at physical chunk c ^ kswz(k), so the lanes of one LDS cycle of the
+//   score MFMA's operand read (consecutive keys, same chunk) hit distinct banks.
+// V tile: KT rows x D bf16 in 32-byte slots (16 d values); logical slot s of
+//   key row k sits at physical slot s ^ vswz(k).  The PV operand is read with
+//   the LDS transpose load (ds_read_b64_tr_b16): in each 16-lane group, lanes
+//   4e..4e+3 address 8 consecutive bytes (4 d values) of key row e and lane i
+//   receives the 4 keys' values of its own d.  vswz spreads the 4 key rows and
+//   the 2 neighbouring slots read in one cycle over distinct banks.
+// Both tiles are filled by direct global->LDS loads: one wave instruction
+//   writes a contiguous 1 KB segment (16 bytes per lane, lane order), so each
+//   lane fetches the global chunk whose swizzled position is its lane slot.
 template <int D>
 __device__ __forceinline__ int kswz(int key) {
     return D == 128 ? (key & 15) : ((key >> 1) & 7);
 }
-__device__ __forceinline__ int vswz(int d) { return (d >> 1) & 7; }
+template <int D>
+__device__ __forceinline__ int vswz(int key) {
+    return D == 128 ? ((key & 3) << 1) : (((key >> 1) & 1) << 1);
+}
 
 template <int D>
 struct TileSmem {
     u32x4 k[2][KT * D / 8];
-    u32x4 v[2][D * KT / 8];
+    u32x4 v[2][KT * D / 8];
 };
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 64-bit LDS transpose read (see the V tile layout above), issued as inline
+// assembly: the compiler's builtin for it carries no memory-alias information,
+// so the waitcnt pass would otherwise wait for every in-flight global->LDS
+// load (of the other LDS buffer) before it.  The caller waits with
+// lds_wait_tr() before using the results.
+template <int OFS>
+__device__ __forceinline__ u32x2 lds_read_tr16(uint32_t lds_addr) {
+    static_assert(OFS >= 0 && OFS < 65536, "DS offset is 16 bits");
+    u32x2 v;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(lds_addr), "i"(OFS) : "memory");
+    return v;
+}
+
+// LDS address (byte offset in the workgroup's LDS) of a shared-memory pointer.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const lds_void*)(p);
+}
+
+// Wait for all outstanding LDS reads; ties the values so that their uses
+// cannot be scheduled above the wait.  LDS operations complete in order, so
+// the extra wait never weakens the compiler's own lgkmcnt accounting.
+template <int N>
+__device__ __forceinline__ void lds_wait_tr(u32x2 (&v)[N]) {
+    static_assert(N == 8, "one d-tile of PV operands");
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]),
+                   "+v"(v[6]), "+v"(v[7])
+                 :
+                 : "memory");
+}
+
+// Direct global -> LDS load of 16 bytes per lane into the wave's 1 KB segment.
+__device__ __forceinline__ void load_lds16(const void* gsrc, void* lds_segment) {
+    __builtin_amdgcn_global_load_lds(gsrc, (lds_void*)lds_segment, 16, 0, 0);
+}
 
 // ---------------------------------------------------------------------------
 // Attention forward
@@ -120,16 +170,18 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     __bf16* __restrict__ O, float* __restrict__ LSE, const int32_t* __restrict__ row_ptr,
     const int32_t* __restrict__ col_idx, int64_t nnz, int32_t n, int32_t NB, int32_t batch_hkv,
     int32_t Hkv, float c_log2) {
-    constexpr int NT = NW * 64;
     constexpr int ROWS = NW * 32;             // stacked query rows per workgroup
     constexpr int NCHUNK = (G * BW + ROWS - 1) / ROWS;
     constexpr int NSUB = BW / KT;             // LDS tiles per key block
-    constexpr int DCH = D / 8;                // 16-byte chunks per K row
-    constexpr int KS = D / 16;                // MFMA k-steps for S
+    constexpr int KS = D / 16;                // MFMA k-steps of the score product
     constexpr int DT = D / 32;                // 32-wide d tiles of O
+    constexpr int RB = D * 2;                 // bytes per key row in LDS
+    constexpr int TILE_B = KT * RB;           // bytes per K (or V) tile
+    constexpr int SEGS = TILE_B / 1024;       // 1 KB direct-load segments per tile
+    constexpr int ROWS_PER_SEG = 1024 / RB;
+    constexpr int SEG_PER_WAVE = SEGS / NW;
     static_assert(ROWS * NCHUNK == G * BW, "rows must tile the stacked group");
-    static_assert((KT * DCH) % NT == 0, "K tile chunks must split evenly");
-    static_assert((16 * DCH) % NT == 0 || NT % (16 * DCH) == 0, "V jobs must split");
+    static_assert(SEGS % NW == 0, "segments must split over the waves");
 
     __shared__ TileSmem<D> sm;
 
@@ -173,92 +225,105 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     }
 
     // ---- route walk ---------------------------------------------------------
-    int32_t pos, pos_end;
+    int32_t pos_end, cur_p;
     if (DENSE) {
-        pos = 0;
+        cur_p = 0;
         pos_end = j + 1;
     } else {
         int64_t e0 = row_ptr[j], e1 = row_ptr[j + 1];
         e0 = e0 < 0 ? 0 : (e0 > nnz ? nnz : e0);
         e1 = e1 < e0 ? e0 : (e1 > nnz ? nnz : e1);
-        pos = (int32_t)e0;
+        cur_p = (int32_t)e0;
         pos_end = (int32_t)e1;
     }
-    // Advance (p, u) to the next tile that exists: a valid block i in [0, j]
-    // whose sub-tile u starts before n.  All quantities fit in 32 bits
-    // (i * BW < n + BW < 2^31).
-    auto seek = [&](int32_t& p, int& u, int32_t& i) -> bool {
-        for (; p < pos_end; ++p, u = 0) {
-            i = DENSE ? p : col_idx[p];
+    int cur_u = 0;
+    // Next tile of the route: a block i in [0, j] (caller tables may hold
+    // anything else; such entries are skipped) and a 64-key sub-tile of it
+    // that starts before n.  All quantities fit in 32 bits.
+    auto next_tile = [&](int32_t& ti, int& tu) -> bool {
+        for (; cur_p < pos_end; ++cur_p, cur_u = 0) {
+            const int32_t i = DENSE ? cur_p : col_idx[cur_p];
             if (i < 0 || i > j) continue;
-            for (; u < NSUB; ++u)
-                if (i * BW + u * KT < n) return true;
+            for (; cur_u < NSUB; ++cur_u)
+                if (i * BW + cur_u * KT < n) {
+                    ti = i;
+                    tu = cur_u++;
+                    return true;
+                }
         }
         return false;
     };
 
-    // ---- global -> register staging of one K/V tile ------------------------
-    constexpr int KLD = KT * DCH / NT;                              // K chunks per thread
-    constexpr int VJOBS = 16 * DCH;                                 // (4 keys x 8 d) jobs
-    constexpr int VLD = VJOBS >= NT ? VJOBS / NT : 1;
-    u32x4 kreg[KLD];
-    u32x4 vreg[VLD][4];
-
+    // ---- direct global -> LDS staging --------------------------------------
     // Keys at or past n occur only in the self block of the last query block,
     // where every query that exists sees them with probability exactly 0.
-    // Their rows are therefore loaded from a clamped, valid row of the same
-    // tile (finite data, 0 * finite = 0) instead of being zeroed, so the
-    // loaded registers are never touched before they are stored to LDS and
-    // the loads stay in flight across the compute of the current tile.
-    auto load_tile = [&](int32_t i, int u) {
+    // Their rows are loaded from a clamped, valid row of the same tile
+    // (finite data, 0 * finite = 0) instead of being zeroed.
+    const int lrow = lane / (RB / 16);   // row inside a 1 KB segment
+    const int pc = lane % (RB / 16);     // physical 16-byte chunk in the row
+    uint32_t kgo[SEG_PER_WAVE], vgo[SEG_PER_WAVE];  // lane byte offsets inside a tile
+#pragma unroll
+    for (int it = 0; it < SEG_PER_WAVE; ++it) {
+        const int row = (it * NW + wave) * ROWS_PER_SEG + lrow;
+        kgo[it] = row * RB + (pc ^ kswz<D>(row)) * 16;
+        vgo[it] = row * RB + (2 * ((pc >> 1) ^ vswz<D>(row)) + (pc & 1)) * 16;
+    }
+    auto load_kv = [&](bool do_k, int kbuf, int vbuf, const __bf16* src_h, int32_t i, int u) {
         const int32_t key0 = i * BW + u * KT;
-        const __bf16* kb = Kh + (int64_t)key0 * D;
-        const __bf16* vb = Vh + (int64_t)key0 * D;
-        const int32_t last = n - key0 - 1;  // last valid row of the tile (>= 0)
+        const char* base = reinterpret_cast<const char*>(src_h + (int64_t)key0 * D);
+        const int32_t last = n - key0 - 1;
+        if (last >= KT - 1) {  // whole tile inside the sequence
 #pragma unroll
-        for (int it = 0; it < KLD; ++it) {
-            const int idx = tid + it * NT;
-            const int kr = min(idx / DCH, last), c = idx % DCH;
-            kreg[it] = *reinterpret_cast<const u32x4*>(kb + kr * D + c * 8);
-        }
+            for (int it = 0; it < SEG_PER_WAVE; ++it) {
+                const int seg = it * NW + wave;
+                if (do_k) load_lds16(base + kgo[it], &sm.k[kbuf][seg * 64]);
+                else load_lds16(base + vgo[it], &sm.v[vbuf][seg * 64]);
+            }
+        } else {
 #pragma unroll
-        for (int it = 0; it < VLD; ++it) {
-            const int job = (VJOBS % NT == 0) ? tid + it * NT : (tid % VJOBS);
-            const int kg = job & 15, dc = job >> 4;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int kr = min(4 * kg + q, last);
-                vreg[it][q] = *reinterpret_cast<const u32x4*>(vb + kr * D + dc * 8);
+            for (int it = 0; it < SEG_PER_WAVE; ++it) {
+                const int seg = it * NW + wave;
+                const int row = seg * ROWS_PER_SEG + lrow;
+                const int shift = (row - min(row, last)) * RB;  // clamp to the last valid row
+                if (do_k) load_lds16(base + kgo[it] - shift, &sm.k[kbuf][seg * 64]);
+                else load_lds16(base + vgo[it] - shift, &sm.v[vbuf][seg * 64]);
             }
         }
     };
+    auto load_k = [&](int kbuf, int32_t i, int u) { load_kv(true, kbuf, 0, Kh, i, u); };
+    auto load_v = [&](int vbuf, int32_t i, int u) { load_kv(false, 0, vbuf, Vh, i, u); };
 
-    auto store_tile = [&](int buf) {
+    // ---- lane-constant LDS read offsets -------------------------------------
+    // Score operand: key row 32 kt + col, logical chunk 2 ks + half.  kswz
+    // depends only on col, so kt adds a constant 32 rows.
+    int kofs[KS];
 #pragma unroll
-        for (int it = 0; it < KLD; ++it) {
-            const int idx = tid + it * NT;
-            const int kr = idx / DCH, c = idx % DCH;
-            sm.k[buf][kr * DCH + (c ^ kswz<D>(kr))] = kreg[it];
-        }
-        u32x2* vt = reinterpret_cast<u32x2*>(&sm.v[buf][0]);
+    for (int ks = 0; ks < KS; ++ks) kofs[ks] = col * RB + 16 * ((2 * ks + half) ^ kswz<D>(col));
+    // PV operand (transpose reads): group gq = lane/16 covers d 32 dt + 16 (gq%2)
+    // .. +15 and keys 16 t + 4 (gq/2) + e (+8 for the second read); vswz of
+    // those rows does not depend on t, so t and the +8 are constant offsets.
+    const int gq = lane >> 4, kk = lane & 15;
+    const int r0 = 4 * (gq >> 1) + (kk >> 2);
+    int vofs[DT];
 #pragma unroll
-        for (int it = 0; it < VLD; ++it) {
-            const int job = (VJOBS % NT == 0) ? tid + it * NT : (tid % VJOBS);
-            const int kg = job & 15, dc = job >> 4;
-            const int lchunk = 2 * (kg >> 2) + (kg & 1);  // logical 16-B chunk of the 4 keys
-            const int hsel = (kg >> 1) & 1;                // which 8-B half of it
+    for (int dt = 0; dt < DT; ++dt)
+        vofs[dt] = r0 * RB + 32 * ((2 * dt + (gq & 1)) ^ vswz<D>(r0)) + 8 * (kk & 3);
+
+    auto score_mfma = [&](auto kbuf_c, f32x16 (&s)[2]) {
+        constexpr int KB = decltype(kbuf_c)::value;
+        const char* kb = reinterpret_cast<const char*>(&sm.k[KB][0]);
 #pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                const uint32_t w0 = vreg[it][0][p], w1 = vreg[it][1][p];
-                const uint32_t w2 = vreg[it][2][p], w3 = vreg[it][3][p];
-                // row d = 8 dc + 2p (low halves) and 8 dc + 2p + 1 (high halves)
-                const u32x2 lo = {(w0 & 0xffffu) | (w1 << 16), (w2 & 0xffffu) | (w3 << 16)};
-                const u32x2 hi = {(w0 >> 16) | (w1 & 0xffff0000u), (w2 >> 16) | (w3 & 0xffff0000u)};
-                const int d0 = 8 * dc + 2 * p, d1 = d0 + 1;
-                vt[2 * (d0 * 8 + (lchunk ^ vswz(d0))) + hsel] = lo;
-                vt[2 * (d1 * 8 + (lchunk ^ vswz(d1))) + hsel] = hi;
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) s[kt][r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt) {
+                const u32x4 w = *reinterpret_cast<const u32x4*>(kb + kofs[ks] + kt * 32 * RB);
+                s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w),
+                                                                qf[ks], s[kt], 0, 0, 0);
             }
-        }
     };
 
     // ---- accumulators -------------------------------------------------------
@@ -267,36 +332,59 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     for (int t = 0; t < DT; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
-    float m_run = -1e30f;     // running max, log2 units (finite: masked scores give 0)
-    float l_run = 0.f;        // this lane's partial row sum (its 32 keys of each tile)
+    float m_run = -1e30f;  // running max, log2 units (finite: masked scores give 0)
+    float l_run = 0.f;     // this lane's partial row sum (its 32 keys of each tile)
 
-    auto compute_tile = [&](int buf, int32_t i, int u) {
-        const bool diag = (i == j);
-        const int kin = u * KT;  // first key position of the tile inside block i
-        if (diag && kin > p0 + 31) return;  // every key is in this wave's future
-        f32x16 s[2];
+    // ---- prologue: K0, V0 and K1 resident, S0 computed ----------------------
+    int32_t ti0 = 0, ti1 = 0, ti2 = 0;
+    int tu0 = 0, tu1 = 0, tu2 = 0;
+    if (!next_tile(ti0, tu0)) {
+        // A row with no usable key block (possible only for a caller route
+        // table): O = 0, LSE = -inf.
+        if (qvalid) {
+            __bf16* Orow = O + (((int64_t)beta * Hq + head) * (int64_t)n + qpos) * D;
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) s[kt][r] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-            for (int kt = 0; kt < 2; ++kt) {
-                const int kr = 32 * kt + col;
-                const u32x4 w = sm.k[buf][kr * DCH + ((2 * ks + half) ^ kswz<D>(kr))];
-                s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w),
-                                                                qf[ks], s[kt], 0, 0, 0);
-            }
+            for (int c = 0; c < D / 2; c += 8)
+                *reinterpret_cast<u32x4*>(Orow + half * (D / 2) + c) = u32x4{0u, 0u, 0u, 0u};
+            if (LSE != nullptr && half == 0)
+                LSE[((int64_t)beta * Hq + head) * (int64_t)n + qpos] = -INFINITY;
         }
-        if (diag) {
-            const int qin = p0 + col;  // query position inside the block
+        return;
+    }
+    bool h1 = next_tile(ti1, tu1);
+    load_k(0, ti0, tu0);
+    load_v(0, ti0, tu0);
+    if (h1) load_k(1, ti1, tu1);
+    __builtin_amdgcn_s_waitcnt(VMCNT0);
+    __syncthreads();
+    f32x16 s_a[2], s_b[2];
+    score_mfma(std::integral_constant<int, 0>{}, s_a);
+
+    // ---- steady state --------------------------------------------------------
+    // Iteration k: tile k's scores are in s_cur, K_k+1 and V_k are resident.
+    //   loads:  K_k+2 -> the K buffer of tile k, V_k+1 -> the other V buffer
+    //   (A) mask, row max and (rare) rescale of tile k
+    //   (B) scores of tile k+1 on the matrix cores, interleaved with the
+    //       exponentials of tile k on the vector ALU
+    //   (C) O += V_k P_k and the row sums of P_k
+    const uint32_t v_lds = lds_addr(&sm.v[0][0]);
+    // One pipeline step; PAR is the buffer parity of tile k (static, so every
+    // LDS read below is a lane-constant base plus an immediate offset).
+    auto step = [&](auto par_c, f32x16 (&s_cur)[2], f32x16 (&s_nxt)[2]) -> bool {
+        constexpr int PAR = decltype(par_c)::value;
+        const bool h2 = h1 && next_tile(ti2, tu2);
+        if (h2) load_k(PAR, ti2, tu2);
+        if (h1) load_v(PAR ^ 1, ti1, tu1);
+
+        // (A)
+        if (ti0 == j) {  // self block: token-level causal triangle
+            const int kin = tu0 * KT, qin = p0 + col;
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int kp = kin + 32 * kt + 8 * (r >> 2) + 4 * half + (r & 3);
-                    if (kp > qin) s[kt][r] = -INFINITY;
+                    if (kp > qin) s_cur[kt][r] = -INFINITY;
                 }
         }
         // Online softmax in the log2 domain (c_log2 = scale * log2 e).  A row's
@@ -310,7 +398,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][r]);
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_cur[kt][r]);
         mx = fmaxf(mx, __shfl_xor(mx, 32));
         const float m_cand = mx * c_log2;
         const bool need = m_cand > m_run + RESCALE_LOG2;
@@ -323,72 +411,84 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[t][r] *= alpha;
         }
-        float ls = 0.f;
+
+        // (B) scores of tile k+1 (unused after the last tile) on the matrix
+        // cores, software-pipelined by hand with the exponentials of tile k:
+        // step q issues score MFMA q, prefetches the K operand of MFMA q+3,
+        // and computes two elements of P_k (fma, exp2, sum; bf16 pack every
+        // fourth step).  sched_barrier pins the order so that the vector work
+        // runs in the shadow of the matrix cores.  The row sum is taken before
+        // the bf16 rounding of P (so the LSE keeps fp32 accuracy).
+        constexpr int NS = 2 * KS;       // score MFMAs of one tile
+        constexpr int EPS = 32 / NS;     // P elements per step
+        static_assert(32 % NS == 0, "P elements must split over the steps");
+        const char* kbn = reinterpret_cast<const char*>(&sm.k[PAR ^ 1][0]);
+        u32x4 kop[4];
+#pragma unroll
+        for (int q = 0; q < 3; ++q)
+            kop[q] = *reinterpret_cast<const u32x4*>(kbn + kofs[q >> 1] + (q & 1) * 32 * RB);
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float p = __builtin_amdgcn_exp2f(fmaf(s[kt][r], c_log2, -m_run));
-                s[kt][r] = p;
-                ls += p;
-            }
-        l_run += ls;
-        // O^T += V^T P^T
+            for (int r = 0; r < 16; ++r) s_nxt[kt][r] = 0.f;
         bf16x8 pb[4];
+        f32x8 pf;
+        float ls0 = 0.f, ls1 = 0.f;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            f32x8 pf;
+        for (int q = 0; q < NS; ++q) {
+            if (q + 3 < NS)
+                kop[(q + 3) & 3] = *reinterpret_cast<const u32x4*>(kbn + kofs[(q + 3) >> 1] +
+                                                                  ((q + 3) & 1) * 32 * RB);
+            s_nxt[q & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, kop[q & 3]), qf[q >> 1], s_nxt[q & 1], 0, 0, 0);
 #pragma unroll
-            for (int m = 0; m < 8; ++m) pf[m] = s[t >> 1][8 * (t & 1) + m];
-            pb[t] = __builtin_convertvector(pf, bf16x8);
+            for (int e = 0; e < EPS; ++e) {
+                const int el = q * EPS + e;  // element of s_cur in P order
+                const float p = __builtin_amdgcn_exp2f(
+                    fmaf(s_cur[el >> 4][el & 15], c_log2, -m_run));
+                pf[el & 7] = p;
+                if (e & 1) ls1 += p; else ls0 += p;
+            }
+            if (((q + 1) * EPS) % 8 == 0) pb[((q + 1) * EPS) / 8 - 1] = __builtin_convertvector(pf, bf16x8);
+            __builtin_amdgcn_sched_barrier(0);
         }
+        l_run += ls0 + ls1;
+
+        // (C) O^T += V^T P^T
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-            const int d = 32 * dt + col;
+            const uint32_t va_base = v_lds + vofs[dt];
+            u32x2 va[8];
+            constexpr int VB = PAR * TILE_B;
+            va[0] = lds_read_tr16<VB + 0 * RB>(va_base);
+            va[1] = lds_read_tr16<VB + 8 * RB>(va_base);
+            va[2] = lds_read_tr16<VB + 16 * RB>(va_base);
+            va[3] = lds_read_tr16<VB + 24 * RB>(va_base);
+            va[4] = lds_read_tr16<VB + 32 * RB>(va_base);
+            va[5] = lds_read_tr16<VB + 40 * RB>(va_base);
+            va[6] = lds_read_tr16<VB + 48 * RB>(va_base);
+            va[7] = lds_read_tr16<VB + 56 * RB>(va_base);
+            lds_wait_tr(va);
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                const u32x4 w = sm.v[buf][d * 8 + ((2 * t + half) ^ vswz(d))];
+                const u32x4 w = {va[2 * t][0], va[2 * t][1], va[2 * t + 1][0], va[2 * t + 1][1]};
                 acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w),
                                                                   pb[t], acc[dt], 0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_waitcnt(VMCNT0);  // this wave's loads have landed
+        __syncthreads();                      // ... and every other wave's
+        if (!h1) return false;
+        ti0 = ti1;
+        tu0 = tu1;
+        ti1 = ti2;
+        tu1 = tu2;
+        h1 = h2;
+        return true;
     };
-
-    // ---- software pipeline: global loads of tile k+1 overlap compute of k ---
-    int32_t cur_p = pos, cur_i = 0;
-    int cur_u = 0;
-    if (!seek(cur_p, cur_u, cur_i)) {
-        // A row with no usable key block (possible only for a caller route
-        // table): O = 0, LSE = -inf.
-        if (qvalid) {
-            __bf16* Orow = O + (((int64_t)beta * Hq + head) * (int64_t)n + qpos) * D;
-#pragma unroll
-            for (int c = 0; c < D / 2; c += 8)
-                *reinterpret_cast<u32x4*>(Orow + half * (D / 2) + c) = u32x4{0u, 0u, 0u, 0u};
-            if (LSE != nullptr && half == 0)
-                LSE[((int64_t)beta * Hq + head) * (int64_t)n + qpos] = -INFINITY;
-        }
-        return;
+    while (step(std::integral_constant<int, 0>{}, s_a, s_b) &&
+           step(std::integral_constant<int, 1>{}, s_b, s_a)) {
     }
-    load_tile(cur_i, cur_u);
-    store_tile(0);
-    __syncthreads();
-    int buf = 0;
-    bool have = true;
-    do {
-        int32_t nxt_p = cur_p, nxt_i = 0;
-        int nxt_u = cur_u + 1;
-        const bool have_n = seek(nxt_p, nxt_u, nxt_i);
-        if (have_n) load_tile(nxt_i, nxt_u);
-        compute_tile(buf, cur_i, cur_u);
-        if (have_n) store_tile(buf ^ 1);
-        __syncthreads();
-        buf ^= 1;
-        cur_p = nxt_p;
-        cur_u = nxt_u;
-        cur_i = nxt_i;
-        have = have_n;
-    } while (have);
 
     // ---- epilogue: O = acc / l, LSE = (m + log2 l) ln 2 ---------------------
     const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -398,11 +498,11 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int gq = 0; gq < 4; ++gq) {
+        for (int gq4 = 0; gq4 < 4; ++gq4) {
             f32x4 v4;
 #pragma unroll
-            for (int c = 0; c < 4; ++c) v4[c] = acc[dt][4 * gq + c] * inv;
-            *reinterpret_cast<bf16x4*>(Orow + 32 * dt + 8 * gq + 4 * half) =
+            for (int c = 0; c < 4; ++c) v4[c] = acc[dt][4 * gq4 + c] * inv;
+            *reinterpret_cast<bf16x4*>(Orow + 32 * dt + 8 * gq4 + 4 * half) =
                 __builtin_convertvector(v4, bf16x4);
         }
     if (LSE != nullptr && half == 0)
