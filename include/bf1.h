@@ -32,7 +32,8 @@
  *    Q, K, V, O must be 16-byte aligned; LSE 4-byte aligned.
  *    q-head h reads kv-head h / (Hq / Hkv) (contiguous GQA groups).
  *  - Supported by the attention kernels: head_dim in {64, 128},
- *    B in {64, 128}, Hq / Hkv in {1, 2, 4, 8}, L >= 0, n >= 0, batch >= 0.
+ *    B in {64, 128}, Hq / Hkv in {1, 2, 4, 8}, L >= 0, 0 <= n < 2^24,
+ *    batch >= 0.
  *    Other values return BF1_ERR_UNSUPPORTED.  n == 0 or batch == 0 is a
  *    no-op returning BF1_OK.
  */

@@ -44,6 +44,8 @@ int check_attn(const void* Q, const void* K, const void* V, void* O, float* LSE,
     if (batch < 0 || n < 0 || Hq < 1 || Hkv < 1) return BF1_ERR_INVALID_ARG;
     if (Hq % Hkv != 0) return BF1_ERR_INVALID_ARG;
     if (n > 0x7fffffffLL - 256) return BF1_ERR_INVALID_ARG;
+    // one head's K or V rows are addressed through a 32-bit buffer range
+    if (n >= (int64_t(1) << 24)) return BF1_ERR_UNSUPPORTED;
     const int32_t G = Hq / Hkv;
     if (head_dim != 64 && head_dim != 128) return BF1_ERR_UNSUPPORTED;
     if (G != 1 && G != 2 && G != 4 && G != 8) return BF1_ERR_UNSUPPORTED;

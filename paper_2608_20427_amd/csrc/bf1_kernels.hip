@@ -50,6 +50,7 @@ constexpr int KT = 64;  // keys per LDS tile
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 constexpr float RESCALE_LOG2 = 8.0f;  // lazy-rescale threshold (log2 units)
+constexpr int KPF = 3;                // K operand reads in flight ahead of the score MFMAs
 constexpr int VMCNT0 = 0x0F70;        // s_waitcnt vmcnt(0) (expcnt, lgkmcnt unconstrained)
 
 // ---------------------------------------------------------------------------
@@ -124,40 +125,67 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-// 64-bit LDS transpose read (see the V tile layout above), issued as inline
-// assembly: the compiler's builtin for it carries no memory-alias information,
-// so the waitcnt pass would otherwise wait for every in-flight global->LDS
-// load (of the other LDS buffer) before it.  The caller waits with
-// lds_wait_tr() before using the results.
-template <int OFS>
-__device__ __forceinline__ u32x2 lds_read_tr16(uint32_t lds_addr) {
-    static_assert(OFS >= 0 && OFS < 65536, "DS offset is 16 bits");
-    u32x2 v;
-    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(lds_addr), "i"(OFS) : "memory");
-    return v;
-}
-
 // LDS address (byte offset in the workgroup's LDS) of a shared-memory pointer.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(const lds_void*)(p);
 }
 
-// Wait for all outstanding LDS reads; ties the values so that their uses
-// cannot be scheduled above the wait.  LDS operations complete in order, so
-// the extra wait never weakens the compiler's own lgkmcnt accounting.
-template <int N>
-__device__ __forceinline__ void lds_wait_tr(u32x2 (&v)[N]) {
-    static_assert(N == 8, "one d-tile of PV operands");
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]),
-                   "+v"(v[6]), "+v"(v[7])
-                 :
-                 : "memory");
+// Eight 64-bit LDS transpose reads (see the V tile layout above) at constant
+// offsets O0 + k * STEP from one lane address, followed by the wait for them,
+// all in ONE inline-assembly statement.  Keeping the wait inside the statement
+// matters: the hardware writes the destination registers asynchronously, so
+// the compiler must not see the values (or be free to reuse or copy their
+// registers) before they have landed; the early-clobber outputs also keep
+// them apart from the address register.  Inline assembly is used because the
+// compiler's builtin for this instruction carries no memory-alias information
+// and would make it wait for every in-flight buffer->LDS load of the other
+// LDS buffer first.  LDS operations complete in order, so the extra wait never
+// weakens the compiler's own lgkmcnt accounting.
+template <int O0, int STEP>
+__device__ __forceinline__ void lds_read_tr16_x8(uint32_t addr, u32x2 (&v)[8]) {
+    static_assert(O0 >= 0 && O0 + 7 * STEP < 65536, "DS offsets are 16 bits");
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %8 offset:%9\n\t"
+        "ds_read_b64_tr_b16 %1, %8 offset:%10\n\t"
+        "ds_read_b64_tr_b16 %2, %8 offset:%11\n\t"
+        "ds_read_b64_tr_b16 %3, %8 offset:%12\n\t"
+        "ds_read_b64_tr_b16 %4, %8 offset:%13\n\t"
+        "ds_read_b64_tr_b16 %5, %8 offset:%14\n\t"
+        "ds_read_b64_tr_b16 %6, %8 offset:%15\n\t"
+        "ds_read_b64_tr_b16 %7, %8 offset:%16\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]),
+          "=&v"(v[6]), "=&v"(v[7])
+        : "v"(addr), "i"(O0), "i"(O0 + STEP), "i"(O0 + 2 * STEP), "i"(O0 + 3 * STEP),
+          "i"(O0 + 4 * STEP), "i"(O0 + 5 * STEP), "i"(O0 + 6 * STEP), "i"(O0 + 7 * STEP)
+        : "memory");
 }
 
-// Direct global -> LDS load of 16 bytes per lane into the wave's 1 KB segment.
-__device__ __forceinline__ void load_lds16(const void* gsrc, void* lds_segment) {
-    __builtin_amdgcn_global_load_lds(gsrc, (lds_void*)lds_segment, 16, 0, 0);
+// Combine a value with the one held by the lane 32 apart (both lane halves
+// hold the same query row).  v_permlane32_swap exchanges the halves in the
+// vector ALU, with no LDS round trip; both halves get identical results.
+__device__ __forceinline__ float pair_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Buffer resource over one head's [n, D] bf16 rows: reads at byte offsets at
+// or past the end return zero, which the staging below relies on.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t head_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+// Direct buffer -> LDS load of 16 bytes per lane into the wave's 1 KB LDS
+// segment (lane order); voff is the lane's byte offset inside the tile, soff
+// the tile's byte offset inside the head.
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, void* lds_segment,
+                                           uint32_t voff, uint32_t soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds_segment, 16, voff, soff, 0, 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -239,26 +267,41 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     int cur_u = 0;
     // Next tile of the route: a block i in [0, j] (caller tables may hold
     // anything else; such entries are skipped) and a 64-key sub-tile of it
-    // that starts before n.  All quantities fit in 32 bits.
+    // that starts before n.  All quantities fit in 32 bits.  The table entry
+    // at cur_p is fetched one call ahead (pref), so the scalar load latency
+    // is hidden behind a pipeline step.
+    int32_t pref = (!DENSE && cur_p < pos_end) ? col_idx[cur_p] : -1;
+    auto advance = [&]() {
+        ++cur_p;
+        cur_u = 0;
+        if (!DENSE) pref = (cur_p < pos_end) ? col_idx[cur_p] : -1;
+    };
     auto next_tile = [&](int32_t& ti, int& tu) -> bool {
-        for (; cur_p < pos_end; ++cur_p, cur_u = 0) {
-            const int32_t i = DENSE ? cur_p : col_idx[cur_p];
-            if (i < 0 || i > j) continue;
-            for (; cur_u < NSUB; ++cur_u)
-                if (i * BW + cur_u * KT < n) {
-                    ti = i;
-                    tu = cur_u++;
-                    return true;
-                }
+        while (cur_p < pos_end) {
+            const int32_t i = DENSE ? cur_p : pref;
+            if (i >= 0 && i <= j) {
+                for (; cur_u < NSUB; ++cur_u)
+                    if (i * BW + cur_u * KT < n) {
+                        ti = i;
+                        tu = cur_u++;
+                        if (cur_u >= NSUB) advance();
+                        return true;
+                    }
+            }
+            advance();
         }
         return false;
     };
 
-    // ---- direct global -> LDS staging --------------------------------------
+    // ---- direct buffer -> LDS staging ----------------------------------------
     // Keys at or past n occur only in the self block of the last query block,
-    // where every query that exists sees them with probability exactly 0.
-    // Their rows are loaded from a clamped, valid row of the same tile
-    // (finite data, 0 * finite = 0) instead of being zeroed.
+    // where every query that exists sees them with probability exactly 0; the
+    // buffer range check returns zeros for those rows (0 * 0 = 0 in P V, and
+    // the zero scores are masked).  A tile that does not exist is "loaded"
+    // from past the end: all lanes read zeros and no memory is touched.
+    const uint32_t head_bytes = (uint32_t)n * RB;
+    const __amdgpu_buffer_rsrc_t k_rsrc = head_rsrc(Kh, head_bytes);
+    const __amdgpu_buffer_rsrc_t v_rsrc = head_rsrc(Vh, head_bytes);
     const int lrow = lane / (RB / 16);   // row inside a 1 KB segment
     const int pc = lane % (RB / 16);     // physical 16-byte chunk in the row
     uint32_t kgo[SEG_PER_WAVE], vgo[SEG_PER_WAVE];  // lane byte offsets inside a tile
@@ -268,30 +311,19 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
         kgo[it] = row * RB + (pc ^ kswz<D>(row)) * 16;
         vgo[it] = row * RB + (2 * ((pc >> 1) ^ vswz<D>(row)) + (pc & 1)) * 16;
     }
-    auto load_kv = [&](bool do_k, int kbuf, int vbuf, const __bf16* src_h, int32_t i, int u) {
-        const int32_t key0 = i * BW + u * KT;
-        const char* base = reinterpret_cast<const char*>(src_h + (int64_t)key0 * D);
-        const int32_t last = n - key0 - 1;
-        if (last >= KT - 1) {  // whole tile inside the sequence
-#pragma unroll
-            for (int it = 0; it < SEG_PER_WAVE; ++it) {
-                const int seg = it * NW + wave;
-                if (do_k) load_lds16(base + kgo[it], &sm.k[kbuf][seg * 64]);
-                else load_lds16(base + vgo[it], &sm.v[vbuf][seg * 64]);
-            }
-        } else {
-#pragma unroll
-            for (int it = 0; it < SEG_PER_WAVE; ++it) {
-                const int seg = it * NW + wave;
-                const int row = seg * ROWS_PER_SEG + lrow;
-                const int shift = (row - min(row, last)) * RB;  // clamp to the last valid row
-                if (do_k) load_lds16(base + kgo[it] - shift, &sm.k[kbuf][seg * 64]);
-                else load_lds16(base + vgo[it] - shift, &sm.v[vbuf][seg * 64]);
-            }
-        }
+    auto tile_off = [&](bool exists, int32_t i, int u) -> uint32_t {
+        return exists ? (uint32_t)(i * BW + u * KT) * RB : head_bytes;
     };
-    auto load_k = [&](int kbuf, int32_t i, int u) { load_kv(true, kbuf, 0, Kh, i, u); };
-    auto load_v = [&](int vbuf, int32_t i, int u) { load_kv(false, 0, vbuf, Vh, i, u); };
+    auto load_k = [&](int kbuf, uint32_t soff) {
+#pragma unroll
+        for (int it = 0; it < SEG_PER_WAVE; ++it)
+            load_lds16(k_rsrc, &sm.k[kbuf][(it * NW + wave) * 64], kgo[it], soff);
+    };
+    auto load_v = [&](int vbuf, uint32_t soff) {
+#pragma unroll
+        for (int it = 0; it < SEG_PER_WAVE; ++it)
+            load_lds16(v_rsrc, &sm.v[vbuf][(it * NW + wave) * 64], vgo[it], soff);
+    };
 
     // ---- lane-constant LDS read offsets -------------------------------------
     // Score operand: key row 32 kt + col, logical chunk 2 ks + half.  kswz
@@ -352,56 +384,39 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
         return;
     }
     bool h1 = next_tile(ti1, tu1);
-    load_k(0, ti0, tu0);
-    load_v(0, ti0, tu0);
-    if (h1) load_k(1, ti1, tu1);
+    load_k(0, tile_off(true, ti0, tu0));
+    load_v(0, tile_off(true, ti0, tu0));
+    if (h1) load_k(1, tile_off(true, ti1, tu1));
     __builtin_amdgcn_s_waitcnt(VMCNT0);
     __syncthreads();
-    f32x16 s_a[2], s_b[2];
-    score_mfma(std::integral_constant<int, 0>{}, s_a);
 
-    // ---- steady state --------------------------------------------------------
-    // Iteration k: tile k's scores are in s_cur, K_k+1 and V_k are resident.
-    //   loads:  K_k+2 -> the K buffer of tile k, V_k+1 -> the other V buffer
-    //   (A) mask, row max and (rare) rescale of tile k
-    //   (B) scores of tile k+1 on the matrix cores, interleaved with the
-    //       exponentials of tile k on the vector ALU
-    //   (C) O += V_k P_k and the row sums of P_k
-    const uint32_t v_lds = lds_addr(&sm.v[0][0]);
-    // One pipeline step; PAR is the buffer parity of tile k (static, so every
-    // LDS read below is a lane-constant base plus an immediate offset).
-    auto step = [&](auto par_c, f32x16 (&s_cur)[2], f32x16 (&s_nxt)[2]) -> bool {
-        constexpr int PAR = decltype(par_c)::value;
-        const bool h2 = h1 && next_tile(ti2, tu2);
-        if (h2) load_k(PAR, ti2, tu2);
-        if (h1) load_v(PAR ^ 1, ti1, tu1);
-
-        // (A)
-        if (ti0 == j) {  // self block: token-level causal triangle
-            const int kin = tu0 * KT, qin = p0 + col;
+    // Row statistics of a score tile: the self-block causal mask, then the
+    // row max in log2 units (m_cand) and whether the running max must move.
+    // Online softmax in the log2 domain (c_log2 = scale * log2 e): a row's
+    // running max m_run only moves when a score exceeds it by more than
+    // 2^RESCALE_LOG2; otherwise the stale max is kept for numerator and
+    // denominator alike, which is exact and keeps every p <= 2^RESCALE_LOG2.
+    // The decision is per row (per lane), so a row's arithmetic never depends
+    // on other rows' data; the wave only skips the rescale work when no row
+    // needs it (alpha = 1 exactly for the others).
+    auto tile_stats = [&](f32x16 (&sc)[2], int32_t ti, int tu, float& m_cand) -> bool {
+        if (ti == j) {  // self block: token-level causal triangle
+            const int kin = tu * KT, qin = p0 + col;
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int kp = kin + 32 * kt + 8 * (r >> 2) + 4 * half + (r & 3);
-                    if (kp > qin) s_cur[kt][r] = -INFINITY;
+                    if (kp > qin) sc[kt][r] = -INFINITY;
                 }
         }
-        // Online softmax in the log2 domain (c_log2 = scale * log2 e).  A row's
-        // running max m_run only moves when a score exceeds it by more than
-        // 2^RESCALE_LOG2; otherwise the stale max is kept for numerator and
-        // denominator alike, which is exact and keeps every p <= 2^RESCALE_LOG2.
-        // The decision is per row (per lane), so a row's arithmetic never
-        // depends on other rows' data; the wave only skips the rescale work
-        // when no row needs it (alpha = 1 exactly for the others).
-        float mx = -INFINITY;
+        float mq[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};  // independent chains
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s_cur[kt][r]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_cand = mx * c_log2;
-        const bool need = m_cand > m_run + RESCALE_LOG2;
+        for (int r = 0; r < 16; ++r) mq[r & 3] = fmaxf(mq[r & 3], fmaxf(sc[0][r], sc[1][r]));
+        m_cand = pair_max(fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]))) * c_log2;
+        return m_cand > m_run + RESCALE_LOG2;
+    };
+    auto apply_rescale = [&](bool need, float m_cand) {
         if (__any(need)) {
             const float alpha = need ? __builtin_amdgcn_exp2f(m_run - m_cand) : 1.0f;
             m_run = need ? m_cand : m_run;
@@ -411,71 +426,108 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[t][r] *= alpha;
         }
+    };
 
-        // (B) scores of tile k+1 (unused after the last tile) on the matrix
-        // cores, software-pipelined by hand with the exponentials of tile k:
-        // step q issues score MFMA q, prefetches the K operand of MFMA q+3,
+    f32x16 s_a[2], s_b[2];
+    score_mfma(std::integral_constant<int, 0>{}, s_a);
+    {
+        float mc;
+        const bool nd = tile_stats(s_a, ti0, tu0, mc);
+        apply_rescale(nd, mc);
+    }
+
+    // ---- steady state --------------------------------------------------------
+    // Iteration k: tile k's scores are in s_cur with its statistics applied,
+    // K_k+1 and V_k are resident.
+    //   phase 1: scores of tile k+1 on the matrix cores, interleaved with the
+    //            exponentials of tile k and with the loads of K_k+2 (into the
+    //            K buffer of tile k) and V_k+1 (into the other V buffer)
+    //   phase 2: O += V_k P_k on the matrix cores, interleaved with the mask
+    //            and row max of tile k+1; its (rare) rescale of O follows
+    const uint32_t v_lds = lds_addr(&sm.v[0][0]);
+    // One pipeline step; PAR is the buffer parity of tile k (static, so every
+    // LDS read below is a lane-constant base plus an immediate offset).
+    auto step = [&](auto par_c, f32x16 (&s_cur)[2], f32x16 (&s_nxt)[2]) -> bool {
+        constexpr int PAR = decltype(par_c)::value;
+        const bool h2 = h1 && next_tile(ti2, tu2);
+        // The loads of K_k+2 and V_k+1 are spread over phase 1; a tile that
+        // does not exist reads zeros past the end of the head (no traffic).
+        const uint32_t soff_k2 = tile_off(h2, ti2, tu2);
+        const uint32_t soff_v1 = tile_off(h1, ti1, tu1);
+
+        // phase 1: scores of tile k+1 (unused after the last tile), P of tile
+        // k.  Step q issues score MFMA q, prefetches the K operand of MFMA q+KPF
         // and computes two elements of P_k (fma, exp2, sum; bf16 pack every
         // fourth step).  sched_barrier pins the order so that the vector work
         // runs in the shadow of the matrix cores.  The row sum is taken before
         // the bf16 rounding of P (so the LSE keeps fp32 accuracy).
         constexpr int NS = 2 * KS;       // score MFMAs of one tile
         constexpr int EPS = 32 / NS;     // P elements per step
+        constexpr int NL = 2 * SEG_PER_WAVE;  // direct loads per wave per tile pair
         static_assert(32 % NS == 0, "P elements must split over the steps");
         const char* kbn = reinterpret_cast<const char*>(&sm.k[PAR ^ 1][0]);
-        u32x4 kop[4];
-#pragma unroll
-        for (int q = 0; q < 3; ++q)
-            kop[q] = *reinterpret_cast<const u32x4*>(kbn + kofs[q >> 1] + (q & 1) * 32 * RB);
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) s_nxt[kt][r] = 0.f;
         bf16x8 pb[4];
-        f32x8 pf;
         float ls0 = 0.f, ls1 = 0.f;
+        {
+            u32x4 kop[KPF + 1];
 #pragma unroll
-        for (int q = 0; q < NS; ++q) {
-            if (q + 3 < NS)
-                kop[(q + 3) & 3] = *reinterpret_cast<const u32x4*>(kbn + kofs[(q + 3) >> 1] +
-                                                                  ((q + 3) & 1) * 32 * RB);
-            s_nxt[q & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8, kop[q & 3]), qf[q >> 1], s_nxt[q & 1], 0, 0, 0);
+            for (int q = 0; q < KPF; ++q)
+                kop[q] = *reinterpret_cast<const u32x4*>(kbn + kofs[q >> 1] + (q & 1) * 32 * RB);
 #pragma unroll
-            for (int e = 0; e < EPS; ++e) {
-                const int el = q * EPS + e;  // element of s_cur in P order
-                const float p = __builtin_amdgcn_exp2f(
-                    fmaf(s_cur[el >> 4][el & 15], c_log2, -m_run));
-                pf[el & 7] = p;
-                if (e & 1) ls1 += p; else ls0 += p;
+            for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) s_nxt[kt][r] = 0.f;
+            f32x8 pf;
+#pragma unroll
+            for (int q = 0; q < NS; ++q) {
+                if (q + KPF < NS)
+                    kop[(q + KPF) % (KPF + 1)] = *reinterpret_cast<const u32x4*>(
+                        kbn + kofs[(q + KPF) >> 1] + ((q + KPF) & 1) * 32 * RB);
+                s_nxt[q & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, kop[q % (KPF + 1)]), qf[q >> 1], s_nxt[q & 1], 0, 0, 0);
+#pragma unroll
+                for (int e = 0; e < EPS; ++e) {
+                    const int el = q * EPS + e;  // element of s_cur in P order
+                    const float pv = __builtin_amdgcn_exp2f(
+                        fmaf(s_cur[el >> 4][el & 15], c_log2, -m_run));
+                    pf[el & 7] = pv;
+                    if (e & 1) ls1 += pv; else ls0 += pv;
+                }
+                if (((q + 1) * EPS) % 8 == 0)
+                    pb[((q + 1) * EPS) / 8 - 1] = __builtin_convertvector(pf, bf16x8);
+#pragma unroll
+                for (int li = (q * NL) / NS; li < ((q + 1) * NL) / NS; ++li) {
+                    if (li < SEG_PER_WAVE)
+                        load_lds16(k_rsrc, &sm.k[PAR][(li * NW + wave) * 64], kgo[li], soff_k2);
+                    else
+                        load_lds16(v_rsrc, &sm.v[PAR ^ 1][((li - SEG_PER_WAVE) * NW + wave) * 64],
+                                   vgo[li - SEG_PER_WAVE], soff_v1);
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
-            if (((q + 1) * EPS) % 8 == 0) pb[((q + 1) * EPS) / 8 - 1] = __builtin_convertvector(pf, bf16x8);
-            __builtin_amdgcn_sched_barrier(0);
         }
         l_run += ls0 + ls1;
 
-        // (C) O^T += V^T P^T
+        // phase 2: O^T += V^T P^T (transpose reads of V_k), interleaved with the
+        // statistics of tile k+1
+        bool need = false;
+        float m_cand = 0.f;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
             const uint32_t va_base = v_lds + vofs[dt];
             u32x2 va[8];
             constexpr int VB = PAR * TILE_B;
-            va[0] = lds_read_tr16<VB + 0 * RB>(va_base);
-            va[1] = lds_read_tr16<VB + 8 * RB>(va_base);
-            va[2] = lds_read_tr16<VB + 16 * RB>(va_base);
-            va[3] = lds_read_tr16<VB + 24 * RB>(va_base);
-            va[4] = lds_read_tr16<VB + 32 * RB>(va_base);
-            va[5] = lds_read_tr16<VB + 40 * RB>(va_base);
-            va[6] = lds_read_tr16<VB + 48 * RB>(va_base);
-            va[7] = lds_read_tr16<VB + 56 * RB>(va_base);
-            lds_wait_tr(va);
+            lds_read_tr16_x8<VB, 8 * RB>(va_base, va);
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const u32x4 w = {va[2 * t][0], va[2 * t][1], va[2 * t + 1][0], va[2 * t + 1][1]};
                 acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w),
                                                                   pb[t], acc[dt], 0, 0, 0);
             }
+            if (dt == 0 && h1) need = tile_stats(s_nxt, ti1, tu1, m_cand);
         }
+        if (h1) apply_rescale(need, m_cand);
+
         __builtin_amdgcn_s_waitcnt(VMCNT0);  // this wave's loads have landed
         __syncthreads();                      // ... and every other wave's
         if (!h1) return false;
@@ -491,7 +543,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     }
 
     // ---- epilogue: O = acc / l, LSE = (m + log2 l) ln 2 ---------------------
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float l_tot = pair_sum(l_run);
     if (!qvalid) return;
     const float inv = 1.f / l_tot;
     __bf16* Orow = O + (((int64_t)beta * Hq + head) * (int64_t)n + qpos) * D;
