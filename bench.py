@@ -66,6 +66,12 @@ def parse():
     return ap.parse_args()
 
 
+def kernel_source_hash():
+    import hashlib
+    path = os.path.join(ROOT, "paper_2608_20427_amd", "csrc", "bf1_kernels.hip")
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
 def timed_reps(torch, fn, warmup, reps):
     """Per-launch device times (ms) of fn on the current stream."""
     for _ in range(warmup):
@@ -221,11 +227,13 @@ def main():
     log(f"timed {args.steps} steps: {ms_per_step:.4f} ms/step, attention kernel {attn_ms:.4f} ms")
 
     achieved = flops / (attn_ms * 1e-3) / 1e12
+    # HBM bytes per launch from the committed counter summary, valid only for
+    # the kernel source it was measured on (null once the kernel changed).
     traffic = None
     if os.path.exists(args.traffic_json):
         try:
             t = json.load(open(args.traffic_json))
-            if t.get("workload") == w.name:
+            if t.get("workload") == w.name and t.get("kernel_source_sha256") == kernel_source_hash():
                 traffic = t.get("bytes_per_launch")
         except (OSError, ValueError):
             traffic = None
