@@ -465,6 +465,10 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
         constexpr int EPS = 32 / NS;     // P elements per step
         constexpr int NL = 2 * SEG_PER_WAVE;  // direct loads per wave per tile pair
         static_assert(32 % NS == 0, "P elements must split over the steps");
+        // The exponentials, the bf16 packing and the DMA issue of phase 1 are
+        // the longer instruction stream of the two phases: give it issue
+        // priority over the other workgroup's wave on this SIMD.
+        __builtin_amdgcn_s_setprio(1);
         const char* kbn = reinterpret_cast<const char*>(&sm.k[PAR ^ 1][0]);
         bf16x8 pb[4];
         float ls0 = 0.f, ls1 = 0.f;
@@ -507,6 +511,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
             }
         }
         l_run += ls0 + ls1;
+        __builtin_amdgcn_s_setprio(0);
 
         // phase 2: O^T += V^T P^T (transpose reads of V_k), interleaved with the
         // statistics of tile k+1
@@ -543,10 +548,17 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     }
 
     // ---- epilogue: O = acc / l, LSE = (m + log2 l) ln 2 ---------------------
+    // O goes through LDS so that the global stores are whole rows: the
+    // accumulator holds, per lane, 8-byte pieces of one query row; each wave
+    // writes its 32 x D tile into its own slice of the (now idle) K buffers,
+    // [row][16-byte chunk ^ (row % 16)], then reads back 16 consecutive bytes
+    // per lane, 16 lanes per row, and stores 4 consecutive rows per
+    // instruction.  The last step's barrier ordered every LDS read of the
+    // tiles before this; no other wave touches this slice.
     const float l_tot = pair_sum(l_run);
-    if (!qvalid) return;
     const float inv = 1.f / l_tot;
-    __bf16* Orow = O + (((int64_t)beta * Hq + head) * (int64_t)n + qpos) * D;
+    constexpr int OCH = D / 8;                 // 16-byte chunks per row
+    char* oslice = reinterpret_cast<char*>(&sm.k[0][0]) + wave * 32 * RB;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -554,10 +566,23 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
             f32x4 v4;
 #pragma unroll
             for (int c = 0; c < 4; ++c) v4[c] = acc[dt][4 * gq4 + c] * inv;
-            *reinterpret_cast<bf16x4*>(Orow + 32 * dt + 8 * gq4 + 4 * half) =
+            const int ch = (4 * dt + gq4) ^ (col % OCH);
+            *reinterpret_cast<bf16x4*>(oslice + col * RB + ch * 16 + half * 8) =
                 __builtin_convertvector(v4, bf16x4);
         }
-    if (LSE != nullptr && half == 0)
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's O tile is in LDS
+    {
+        const int32_t row0 = j * BW + p0;  // first query of this wave
+        __bf16* Obase = O + (((int64_t)beta * Hq + head) * (int64_t)n + row0) * D;
+        constexpr int RPI = 64 / OCH;      // rows per store instruction
+#pragma unroll
+        for (int it = 0; it < 32 / RPI; ++it) {
+            const int r = it * RPI + lane / OCH, c = lane % OCH;
+            const u32x4 w = *reinterpret_cast<const u32x4*>(oslice + r * RB + ((c ^ (r % OCH)) * 16));
+            if (row0 + r < n) *reinterpret_cast<u32x4*>(Obase + (int64_t)r * D + c * 8) = w;
+        }
+    }
+    if (LSE != nullptr && half == 0 && qvalid)
         LSE[((int64_t)beta * Hq + head) * (int64_t)n + qpos] = (m_run + log2f(l_tot)) * LN2;
 }
 
