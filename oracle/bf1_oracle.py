@@ -27,6 +27,13 @@ Mask (§3.1): the self block j uses a token-level causal triangle (key s is
 visible to query t in the same block iff s <= t); every other selected block
 is strictly earlier and fully visible.  Keys at positions >= n do not exist.
 
+Backward: the gradients of O with respect to Q, K and V for an upstream
+gradient dO, on the same route (the operator the paper trains through,
+§2/§4.1).  With P the masked softmax weights, D_t = sum_s P_ts dP_ts and the
+scale c = 1/sqrt(head_dim), these are the textbook softmax-attention
+gradients: dV = P^T dO, dP = dO V^T, dS = P * (dP - D), dQ = c dS K,
+dK = c dS^T Q, summed over the q-heads of a GQA group for dK and dV.
+
 Attention: softmax with scale 1/sqrt(head_dim) and no score bias (§3.1,
 "no scale-dependent score bias"), restricted to the mask above.  q-head h
 reads kv-head h // (Hq / Hkv) (contiguous GQA groups).  Outputs are O
@@ -51,6 +58,9 @@ __all__ = [
     "attn_gathered_fp64",
     "attn_csr_fp64",
     "dense_causal_fp64",
+    "csr_transposed",
+    "attn_bwd_csr_fp64",
+    "attn_bwd_gathered_fp64",
 ]
 
 
@@ -295,3 +305,106 @@ def dense_causal_fp64(q, k, v, scale=None, rows=None):
                 lse[beta, h, t] = m + np.log(z)
                 out[beta, h, t] = np.exp(x - lse[beta, h, t]) @ v[beta, g, : t + 1]
     return out, lse
+
+
+# ---------------------------------------------------------------------------
+# Backward (gradients of the §3.1 attention with respect to Q, K, V)
+# ---------------------------------------------------------------------------
+
+def csr_transposed(n, b, L=2):
+    """Transposed route: for every key block i, the ascending query blocks j
+    that select it (i in P(j), Eq. 1), as CSR (row_ptr[NB+1], col_idx).
+    Built by inverting the enumerated route table."""
+    NB = num_blocks(n, b)
+    users = [[] for _ in range(NB)]
+    for j, sel in enumerate(route_table(n, b, L)):
+        for i in sel:
+            users[i].append(j)
+    row_ptr = np.zeros(NB + 1, dtype=np.int64)
+    for i in range(NB):
+        row_ptr[i + 1] = row_ptr[i] + len(users[i])
+    col_idx = np.array([j for u in users for j in sorted(u)], dtype=np.int64)
+    return row_ptr.astype(np.int32), col_idx.astype(np.int32)
+
+
+def attn_bwd_csr_fp64(q, k, v, do, b, row_ptr, col_idx, scale=None, q_blocks=None,
+                      kv_blocks=None):
+    """Gradients (dQ, dK, dV) of the attention over a CSR block route, in
+    float64, for the upstream gradient dO (same layout as O).
+
+    For every query block j the selected key ranges are gathered exactly as
+    in the forward (form ii), the masked softmax weights P are formed, and
+    with D = rowsum(P * dP):
+        dP = dO V^T,  dS = P * (dP - D),
+        dV += P^T dO,  dQ = c dS K,  dK += c dS^T Q.
+    ``q_blocks`` restricts which query blocks' dQ rows are computed and
+    ``kv_blocks`` which key blocks' dK/dV rows are accumulated (all by
+    default); rows not computed are NaN.  Only the query blocks needed for
+    the requested rows are visited.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    batch, Hq, Hkv, n, d = _check_shapes(q, k, v)
+    if do.shape != q.shape:
+        raise ValueError("dO must have the shape of Q")
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    G = Hq // Hkv
+    NB = num_blocks(n, b)
+    qset = set(range(NB)) if q_blocks is None else {int(x) for x in q_blocks}
+    kvset = set(range(NB)) if kv_blocks is None else {int(x) for x in kv_blocks}
+    dq = np.full(q.shape, np.nan)
+    dk = np.full(k.shape, np.nan)
+    dv = np.full(v.shape, np.nan)
+    for j in qset:
+        dq[:, :, j * b:min((j + 1) * b, n)] = 0.0
+    for i in kvset:
+        dk[:, :, i * b:min((i + 1) * b, n)] = 0.0
+        dv[:, :, i * b:min((i + 1) * b, n)] = 0.0
+    for j in range(NB):
+        sel = [int(i) for i in col_idx[row_ptr[j]:row_ptr[j + 1]]]
+        if j not in qset and not kvset.intersection(sel):
+            continue
+        t0, t1 = j * b, min((j + 1) * b, n)
+        keys = np.concatenate([np.arange(i * b, min((i + 1) * b, n)) for i in sel])
+        t = np.arange(t0, t1)[:, None]
+        s = keys[None, :]
+        allowed = (s // b < j) | (s <= t)
+        keep = np.isin(keys // b, list(kvset))  # key rows whose dK/dV are requested
+        for beta in range(batch):
+            for h in range(Hq):
+                g = h // G
+                gq, gk, gv = _bwd_gathered(q[beta, h, t0:t1], k[beta, g, keys], v[beta, g, keys],
+                                           do[beta, h, t0:t1], allowed, scale)
+                if j in qset:
+                    dq[beta, h, t0:t1] = gq
+                if keep.any():
+                    kk = keys[keep]
+                    dv[beta, g, kk] += gv[keep]
+                    dk[beta, g, kk] += gk[keep]
+    return dq, dk, dv
+
+
+def _bwd_gathered(qr, kr, vr, dor, allowed, scale):
+    """Softmax-attention gradients for one set of query rows qr over gathered
+    keys kr / values vr with a boolean mask: returns (dQ rows, dK rows,
+    dV rows) of this row set's contribution."""
+    x = scale * (qr @ kr.T)
+    x = np.where(allowed, x, -np.inf)
+    m = np.max(x, axis=1, keepdims=True)
+    p = np.exp(x - m)
+    p /= np.sum(p, axis=1, keepdims=True)
+    dp = dor @ vr.T
+    delta = np.sum(p * dp, axis=1, keepdims=True)
+    ds = p * (dp - delta)
+    return scale * (ds @ kr), scale * (ds.T @ qr), p.T @ dor
+
+
+def attn_bwd_gathered_fp64(q, k, v, do, b, L=2, scale=None, q_blocks=None, kv_blocks=None):
+    """Backward over the BF1 route of Eq. 1."""
+    n = np.shape(q)[2]
+    row_ptr, col_idx = csr(n, b, L)
+    return attn_bwd_csr_fp64(q, k, v, do, b, row_ptr, col_idx, scale=scale,
+                             q_blocks=q_blocks, kv_blocks=kv_blocks)

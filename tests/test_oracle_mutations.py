@@ -116,3 +116,58 @@ def test_wrong_gqa_map_is_caught(monkeypatch):
 
     monkeypatch.setattr(orc, "attn_csr_fp64", interleaved)
     assert run_pins([(TA.test_gqa_grouping_contiguous, ())])
+
+
+# ---- backward: planted slips in the per-row-set gradient core -------------
+import test_oracle_backward as TB  # noqa: E402
+
+_bwd = orc._bwd_gathered
+
+
+def _bwd_parts(qr, kr, vr, dor, allowed, scale):
+    x = scale * (qr @ kr.T)
+    x = np.where(allowed, x, -np.inf)
+    p = np.exp(x - np.max(x, axis=1, keepdims=True))
+    p /= np.sum(p, axis=1, keepdims=True)
+    dp = dor @ vr.T
+    delta = np.sum(p * dp, axis=1, keepdims=True)
+    return p, dp, delta
+
+
+def bwd_no_delta(qr, kr, vr, dor, allowed, scale):
+    p, dp, _ = _bwd_parts(qr, kr, vr, dor, allowed, scale)
+    ds = p * dp
+    return scale * (ds @ kr), scale * (ds.T @ qr), p.T @ dor
+
+
+def bwd_sign_flip(qr, kr, vr, dor, allowed, scale):
+    p, dp, delta = _bwd_parts(qr, kr, vr, dor, allowed, scale)
+    ds = p * (delta - dp)
+    return scale * (ds @ kr), scale * (ds.T @ qr), p.T @ dor
+
+
+def bwd_dk_unscaled(qr, kr, vr, dor, allowed, scale):
+    p, dp, delta = _bwd_parts(qr, kr, vr, dor, allowed, scale)
+    ds = p * (dp - delta)
+    return scale * (ds @ kr), ds.T @ qr, p.T @ dor
+
+
+def bwd_dv_transposed_weights(qr, kr, vr, dor, allowed, scale):
+    p, dp, delta = _bwd_parts(qr, kr, vr, dor, allowed, scale)
+    ds = p * (dp - delta)
+    w = np.exp(np.where(allowed, scale * (qr @ kr.T), -np.inf))  # unnormalised weights
+    return scale * (ds @ kr), scale * (ds.T @ qr), w.T @ dor
+
+
+BWD_PINS = [
+    (TB.test_backward_matches_finite_differences, (23, 4, 1, 2, 1)),
+    (TB.test_backward_row_sum_invariants, ()),
+    (TB.test_backward_zero_keys_closed_form, ()),
+]
+
+
+@pytest.mark.parametrize("bad", [bwd_no_delta, bwd_sign_flip, bwd_dk_unscaled,
+                                 bwd_dv_transposed_weights])
+def test_backward_mutations_are_caught(monkeypatch, bad):
+    monkeypatch.setattr(orc, "_bwd_gathered", bad)
+    assert run_pins(BWD_PINS)
