@@ -120,8 +120,52 @@ int bf1_dense_causal_fwd(const void* Q, const void* K, const void* V, void* O, f
                          int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
                          void* stream);
 
+/*
+ * Transposed route (host only, no device work): for every key block i the
+ * ascending query blocks j whose route P(j) (§3.1, Eq. 1) contains i -- all
+ * blocks for i = 0 (the global block), otherwise i, its L local successors
+ * and the blocks i + 2^r (r >= 2) below NB.  This is the iteration space of
+ * the dK/dV pass of the backward.
+ *   row_ptr : HOST int32[NB + 1]; col_idx : HOST int32[col_capacity], the
+ *             same nnz as the forward table (bf1_plan_size).
+ * Returns BF1_ERR_BUFFER_TOO_SMALL if col_capacity < nnz.
+ */
+int bf1_plan_transposed(int64_t n, int32_t B, int32_t L,
+                        int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity);
+
+/*
+ * BF1 backward: gradients of O = softmax(mask(Q K^T / sqrt(d))) V with the
+ * §3.1 mask, for an upstream gradient dO, recomputing the weights from the
+ * forward's LSE:
+ *     P = exp(Q K^T / sqrt(d) - LSE),  D = rowsum(dO * O),  dS = P * (dO V^T - D),
+ *     dQ = dS K / sqrt(d),  dK = dS^T Q / sqrt(d),  dV = P^T dO,
+ * dK and dV summed over the q-heads of each GQA group.
+ *   Q, O, dO : [batch, Hq, n, 128] bf16 (O and LSE as written by bf1_attn_fwd)
+ *   K, V     : [batch, Hkv, n, 128] bf16
+ *   LSE      : [batch, Hq, n] fp32, natural log
+ *   dQ       : [batch, Hq, n, 128] fp32 (caller-owned, overwritten)
+ *   dK, dV   : [batch, Hkv, n, 128] fp32 (caller-owned, overwritten)
+ *   workspace: caller-owned device scratch of at least
+ *              bf1_attn_bwd_workspace_size() bytes, 256-byte aligned; its
+ *              contents on entry are irrelevant and are clobbered.
+ * Supported: head_dim 128, B in {64, 128}, G = Hq/Hkv in {1, 2, 4, 8} with
+ * G * B >= 128 (so G = 1 needs B = 128); others return BF1_ERR_UNSUPPORTED.
+ * Three kernels on `stream`: dQ (also writes D to the workspace), dK/dV
+ * over the transposed route (cut into segments of at most 16 query blocks;
+ * the segments of long lists -- block 0 -- leave partial sums in the
+ * workspace), and a fixed-order sum of those partials.  The route and its
+ * transpose are cached per (device, n, B, L) like bf1_attn_fwd's.  The result
+ * is deterministic.
+ */
+int bf1_attn_bwd_workspace_size(int32_t batch, int64_t n, int32_t Hq, int32_t Hkv,
+                                int32_t head_dim, int32_t B, int32_t L, int64_t* bytes);
+int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                 const float* LSE, float* dQ, float* dK, float* dV,
+                 int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                 int32_t B, int32_t L, void* workspace, int64_t workspace_bytes, void* stream);
+
 /* Frees every cached plan (device memory owned by the library).  Must not
- * race with in-flight bf1_attn_fwd calls that use those plans. */
+ * race with in-flight bf1_attn_fwd / bf1_attn_bwd calls that use those plans. */
 void bf1_release_plans(void);
 
 /* Static, human-readable name of a status code. */

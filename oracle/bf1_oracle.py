@@ -61,6 +61,7 @@ __all__ = [
     "csr_transposed",
     "attn_bwd_csr_fp64",
     "attn_bwd_gathered_fp64",
+    "attn_bwd_abs_terms_fp64",
 ]
 
 
@@ -328,7 +329,7 @@ def csr_transposed(n, b, L=2):
 
 
 def attn_bwd_csr_fp64(q, k, v, do, b, row_ptr, col_idx, scale=None, q_blocks=None,
-                      kv_blocks=None):
+                      kv_blocks=None, o=None, _core=None):
     """Gradients (dQ, dK, dV) of the attention over a CSR block route, in
     float64, for the upstream gradient dO (same layout as O).
 
@@ -340,7 +341,10 @@ def attn_bwd_csr_fp64(q, k, v, do, b, row_ptr, col_idx, scale=None, q_blocks=Non
     ``q_blocks`` restricts which query blocks' dQ rows are computed and
     ``kv_blocks`` which key blocks' dK/dV rows are accumulated (all by
     default); rows not computed are NaN.  Only the query blocks needed for
-    the requested rows are visited.
+    the requested rows are visited.  ``o`` (the forward output, same layout as
+    Q) makes D = rowsum(dO * o) instead of the exact rowsum(P * dP): the two
+    agree for the exact o; a given o is what a backward that takes O as an
+    input computes with.
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -349,6 +353,11 @@ def attn_bwd_csr_fp64(q, k, v, do, b, row_ptr, col_idx, scale=None, q_blocks=Non
     batch, Hq, Hkv, n, d = _check_shapes(q, k, v)
     if do.shape != q.shape:
         raise ValueError("dO must have the shape of Q")
+    if o is not None:
+        o = np.asarray(o, dtype=np.float64)
+        if o.shape != q.shape:
+            raise ValueError("o must have the shape of Q")
+    core = _core if _core is not None else _bwd_gathered
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     G = Hq // Hkv
@@ -376,8 +385,9 @@ def attn_bwd_csr_fp64(q, k, v, do, b, row_ptr, col_idx, scale=None, q_blocks=Non
         for beta in range(batch):
             for h in range(Hq):
                 g = h // G
-                gq, gk, gv = _bwd_gathered(q[beta, h, t0:t1], k[beta, g, keys], v[beta, g, keys],
-                                           do[beta, h, t0:t1], allowed, scale)
+                delta = None if o is None else np.sum(do[beta, h, t0:t1] * o[beta, h, t0:t1], axis=1)
+                gq, gk, gv = core(q[beta, h, t0:t1], k[beta, g, keys], v[beta, g, keys],
+                                  do[beta, h, t0:t1], allowed, scale, delta)
                 if j in qset:
                     dq[beta, h, t0:t1] = gq
                 if keep.any():
@@ -387,24 +397,67 @@ def attn_bwd_csr_fp64(q, k, v, do, b, row_ptr, col_idx, scale=None, q_blocks=Non
     return dq, dk, dv
 
 
-def _bwd_gathered(qr, kr, vr, dor, allowed, scale):
-    """Softmax-attention gradients for one set of query rows qr over gathered
-    keys kr / values vr with a boolean mask: returns (dQ rows, dK rows,
-    dV rows) of this row set's contribution."""
+def _bwd_weights(qr, kr, vr, dor, allowed, scale, delta):
+    """Masked softmax weights P, dP = dO V^T and dS = P (dP - D) of one set of
+    query rows over gathered keys (D = rowsum(P dP) unless given)."""
     x = scale * (qr @ kr.T)
     x = np.where(allowed, x, -np.inf)
     m = np.max(x, axis=1, keepdims=True)
     p = np.exp(x - m)
     p /= np.sum(p, axis=1, keepdims=True)
     dp = dor @ vr.T
-    delta = np.sum(p * dp, axis=1, keepdims=True)
-    ds = p * (dp - delta)
+    if delta is None:
+        delta = np.sum(p * dp, axis=1)
+    ds = p * (dp - delta[:, None])
+    return p, ds
+
+
+def _bwd_gathered(qr, kr, vr, dor, allowed, scale, delta=None):
+    """Softmax-attention gradients for one set of query rows qr over gathered
+    keys kr / values vr with a boolean mask: returns (dQ rows, dK rows,
+    dV rows) of this row set's contribution."""
+    p, ds = _bwd_weights(qr, kr, vr, dor, allowed, scale, delta)
     return scale * (ds @ kr), scale * (ds.T @ qr), p.T @ dor
 
 
-def attn_bwd_gathered_fp64(q, k, v, do, b, L=2, scale=None, q_blocks=None, kv_blocks=None):
+def _bwd_abs_terms(qr, kr, vr, dor, allowed, scale, delta=None):
+    """Sums of the magnitudes of the terms of each gradient element:
+    c sum_s |dS||K|, c sum_t |dS||Q|, sum_t P |dO| (same shapes)."""
+    p, ds = _bwd_weights(qr, kr, vr, dor, allowed, scale, delta)
+    a = np.abs(ds)
+    return scale * (a @ np.abs(kr)), scale * (a.T @ np.abs(qr)), p.T @ np.abs(dor)
+
+
+def _bwd_abs_terms_pdp(qr, kr, vr, dor, allowed, scale, delta=None):
+    """As _bwd_abs_terms with |dS| = P |dP - D| replaced by P (|dP| + |D|):
+    the scale of the cancellation in dP - D (dV has no such term: zeros)."""
+    p, _ = _bwd_weights(qr, kr, vr, dor, allowed, scale, delta)
+    dp = dor @ vr.T
+    if delta is None:
+        delta = np.sum(p * dp, axis=1)
+    a = p * (np.abs(dp) + np.abs(delta)[:, None])
+    return scale * (a @ np.abs(kr)), scale * (a.T @ np.abs(qr)), np.zeros((kr.shape[0], dor.shape[1]))
+
+
+def attn_bwd_gathered_fp64(q, k, v, do, b, L=2, scale=None, q_blocks=None, kv_blocks=None,
+                           o=None):
     """Backward over the BF1 route of Eq. 1."""
     n = np.shape(q)[2]
     row_ptr, col_idx = csr(n, b, L)
     return attn_bwd_csr_fp64(q, k, v, do, b, row_ptr, col_idx, scale=scale,
-                             q_blocks=q_blocks, kv_blocks=kv_blocks)
+                             q_blocks=q_blocks, kv_blocks=kv_blocks, o=o)
+
+
+def attn_bwd_abs_terms_fp64(q, k, v, do, b, L=2, scale=None, q_blocks=None, kv_blocks=None,
+                            o=None, kind="ds"):
+    """Term-magnitude sums of the backward over the BF1 route, laid out like
+    (dQ, dK, dV).  kind "ds": c sum_s |dS_ts| |K_s|, c sum_t |dS_ts| |Q_t|,
+    sum_t P_ts |dO_t| -- an implementation that rounds P and dS to bf16
+    (relative error <= 2^-8, 8 significant bits) before the products has
+    element errors bounded by 2^-8 times these.  kind "pdp": the same with |dS| replaced by
+    P (|dP| + |D|), the scale of the fp32 cancellation in dS = P (dP - D)."""
+    n = np.shape(q)[2]
+    row_ptr, col_idx = csr(n, b, L)
+    core = {"ds": _bwd_abs_terms, "pdp": _bwd_abs_terms_pdp}[kind]
+    return attn_bwd_csr_fp64(q, k, v, do, b, row_ptr, col_idx, scale=scale, q_blocks=q_blocks,
+                             kv_blocks=kv_blocks, o=o, _core=core)

@@ -1,4 +1,4 @@
-"""BF1 causal dyadic block-sparse attention (prefill forward) for MI355X.
+"""BF1 causal dyadic block-sparse attention (prefill forward and backward) for MI355X.
 
 Thin ctypes binding over libbf1.so (declared in include/bf1.h).  Every
 function here only checks tensor metadata and marshals pointers, sizes and
@@ -18,6 +18,7 @@ import os
 __all__ = [
     "BF1Error", "lib_path", "load", "version", "status_string", "plan_size", "plan",
     "attn_fwd", "attn_fwd_csr", "dense_causal_fwd", "release_plans", "selected_flops",
+    "plan_transposed", "bwd_workspace_size", "attn_bwd", "selected_bwd_flops",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -70,6 +71,14 @@ def load():
     lib.bf1_dense_causal_fwd.argtypes = attn + [vp]
     lib.bf1_release_plans.restype = None
     lib.bf1_release_plans.argtypes = []
+    lib.bf1_plan_transposed.restype = ctypes.c_int
+    lib.bf1_plan_transposed.argtypes = [i64, i32, i32, vp, vp, i64]
+    lib.bf1_attn_bwd_workspace_size.restype = ctypes.c_int
+    lib.bf1_attn_bwd_workspace_size.argtypes = [i32, i64, i32, i32, i32, i32, i32,
+                                                ctypes.POINTER(i64)]
+    lib.bf1_attn_bwd.restype = ctypes.c_int
+    lib.bf1_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i64, i32, i32, i32,
+                                 i32, i32, vp, i64, vp]
     _LIB = lib
     return lib
 
@@ -185,3 +194,59 @@ def dense_causal_fwd(q, k, v, out=None, lse=None, want_lse=True, stream=None):
 
 def release_plans():
     load().bf1_release_plans()
+
+
+def plan_transposed(n, B=64, L=2):
+    """Transposed route (host only): for every key block, the ascending query
+    blocks whose route selects it, as numpy int32 (row_ptr[NB+1], col_idx)."""
+    import numpy as np
+    nb, nnz, _ = plan_size(n, B, L)
+    row_ptr = np.zeros(nb + 1, dtype=np.int32)
+    col_idx = np.zeros(max(nnz, 1), dtype=np.int32)
+    _check(load().bf1_plan_transposed(int(n), int(B), int(L), row_ptr.ctypes.data_as(ctypes.c_void_p),
+                                      col_idx.ctypes.data_as(ctypes.c_void_p), col_idx.size),
+           "bf1_plan_transposed")
+    return row_ptr, col_idx[:nnz]
+
+
+def bwd_workspace_size(batch, n, Hq, Hkv, d=128, B=64, L=2):
+    """Bytes of device workspace bf1_attn_bwd needs."""
+    out = ctypes.c_int64(0)
+    _check(load().bf1_attn_bwd_workspace_size(int(batch), int(n), int(Hq), int(Hkv), int(d),
+                                              int(B), int(L), ctypes.byref(out)),
+           "bf1_attn_bwd_workspace_size")
+    return out.value
+
+
+def selected_bwd_flops(batch, n, Hq, d, B=64, L=2):
+    """Algorithmic flops of the backward on the selected pairs: the five
+    products S = Q K^T (recomputed), dP = dO V^T, dV = P^T dO, dQ = dS K and
+    dK = dS^T Q, 2 d flops per selected pair each."""
+    return 10 * d * plan_size(n, B, L)[2] * Hq * batch
+
+
+def attn_bwd(q, k, v, o, do, lse, B=64, L=2, dq=None, dk=None, dv=None, workspace=None,
+             stream=None):
+    """BF1 backward; returns float32 (dQ, dK, dV).  o and lse are the
+    forward's outputs; do is the upstream gradient of o (bf16, o's shape)."""
+    import torch
+    out, _, (batch, n, Hq, Hkv, d) = _prep(q, k, v, o, lse, True)
+    if do.shape != q.shape or do.dtype != torch.bfloat16 or not do.is_contiguous() or not do.is_cuda:
+        raise ValueError("do must be a contiguous bf16 CUDA tensor shaped like q")
+    def _grad(t, shape):
+        if t is None:
+            return torch.empty(shape, dtype=torch.float32, device=q.device)
+        if t.shape != shape or t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("gradient buffers must be contiguous float32 tensors")
+        return t
+    dq = _grad(dq, q.shape)
+    dk = _grad(dk, k.shape)
+    dv = _grad(dv, v.shape)
+    need = bwd_workspace_size(batch, n, Hq, Hkv, d, B, L)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
+    _check(load().bf1_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq),
+                               _ptr(dk), _ptr(dv), batch, n, Hq, Hkv, d, int(B), int(L),
+                               _ptr(workspace), workspace.numel(), _stream(stream)),
+           "bf1_attn_bwd")
+    return dq, dk, dv

@@ -3,9 +3,12 @@
 // check happens before any HIP call, so invalid calls touch no device.
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
+#include <array>
 #include <map>
 #include <mutex>
 #include <tuple>
+#include <vector>
 
 #include "../../include/bf1.h"
 #include "bf1_kernels.h"
@@ -62,6 +65,154 @@ int check_attn(const void* Q, const void* K, const void* V, void* O, float* LSE,
 
 int run_attn(const bf1::AttnArgs& a, hipStream_t s) { return status_of(bf1::launch_attention(a, s)); }
 
+// Cached forward route of (current device, n, B, L), built by the planner
+// kernel on first use; `s` is ordered after the planner.
+int get_plan(int64_t n, int32_t B, int32_t L, hipStream_t s, Plan* out) {
+    int64_t NB, nnz;
+    if (!route_sizes(n, B, L, &NB, &nnz)) return BF1_ERR_INVALID_ARG;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return BF1_ERR_HIP;
+    {
+        std::lock_guard<std::mutex> lock(g_mu);
+        auto key = std::make_tuple(dev, n, B, L);
+        auto it = g_plans.find(key);
+        if (it == g_plans.end()) {
+            Plan p;
+            p.nnz = nnz;
+            if (hipMalloc((void**)&p.row_ptr, sizeof(int32_t) * (NB + 1)) != hipSuccess)
+                return BF1_ERR_NOMEM;
+            if (hipMalloc((void**)&p.col_idx, sizeof(int32_t) * (nnz > 0 ? nnz : 1)) != hipSuccess) {
+                (void)hipFree(p.row_ptr);
+                return BF1_ERR_NOMEM;
+            }
+            if (hipEventCreateWithFlags(&p.ready, hipEventDisableTiming) != hipSuccess) {
+                (void)hipFree(p.row_ptr);
+                (void)hipFree(p.col_idx);
+                return BF1_ERR_HIP;
+            }
+            hipError_t e = bf1::launch_plan((int32_t)NB, L, p.row_ptr, p.col_idx, s);
+            if (e == hipSuccess) e = hipEventRecord(p.ready, s);
+            if (e != hipSuccess) {
+                (void)hipFree(p.row_ptr);
+                (void)hipFree(p.col_idx);
+                (void)hipEventDestroy(p.ready);
+                return BF1_ERR_HIP;
+            }
+            it = g_plans.emplace(key, p).first;
+        }
+        *out = it->second;
+    }
+    // The plan may have been built on another stream: order this one after it.
+    if (hipStreamWaitEvent(s, out->ready, 0) != hipSuccess) return BF1_ERR_HIP;
+    return BF1_OK;
+}
+
+// ---- backward plan: transposed route cut into segments ---------------------
+// Every 64-key tile (key block i, sub-tile u, starting before n) gets the list
+// of query blocks that select block i; lists longer than SEG_MAX entries are
+// cut into segments whose partial dK/dV go to numbered workspace slots and are
+// summed by the reduce kernel.  Segments are ordered longest first.
+constexpr int64_t SEG_MAX = 16;
+
+struct BwdLayout {
+    std::vector<int32_t> users, segs, reds;
+    int32_t nslots = 0;
+};
+
+bool bwd_layout(int64_t n, int32_t B, int32_t L, BwdLayout* lay, bool fill) {
+    const int64_t NB = (n + B - 1) / B;
+    const int nsub = B / 64;
+    std::vector<int32_t> tmp;
+    std::vector<std::array<int32_t, 8>> segs;
+    int64_t nslots = 0, total = 0;
+    for (int64_t i = 0; i < NB; ++i) {
+        const int64_t cnt = bf1::route_users(NB, L, i, nullptr);
+        const int64_t off = total;
+        if (fill) {
+            tmp.resize(cnt);
+            bf1::route_users(NB, L, i, tmp.data());
+            lay->users.insert(lay->users.end(), tmp.begin(), tmp.end());
+        }
+        total += cnt;
+        const int64_t nch = (cnt + SEG_MAX - 1) / SEG_MAX;
+        for (int u = 0; u < nsub; ++u) {
+            if (i * B + u * 64 >= n) break;
+            const int64_t slot0 = nch > 1 ? nslots : -1;
+            for (int64_t c = 0; c < nch; ++c) {
+                const int64_t m = std::min(SEG_MAX, cnt - SEG_MAX * c);
+                if (fill)
+                    segs.push_back({(int32_t)i, u, (int32_t)(off + SEG_MAX * c), (int32_t)m,
+                                    (int32_t)(nch > 1 ? slot0 + c : -1), 0, 0, 0});
+            }
+            if (nch > 1) {
+                if (fill) lay->reds.insert(lay->reds.end(), {(int32_t)i, u, (int32_t)slot0, (int32_t)nch});
+                nslots += nch;
+            }
+            if (nslots > 0x3fffffff || total > 0x3fffffff) return false;
+        }
+    }
+    if (fill) {
+        std::stable_sort(segs.begin(), segs.end(),
+                         [](const std::array<int32_t, 8>& a, const std::array<int32_t, 8>& b) {
+                             return a[3] > b[3];
+                         });
+        for (auto& sg : segs) lay->segs.insert(lay->segs.end(), sg.begin(), sg.end());
+    }
+    lay->nslots = (int32_t)nslots;
+    return true;
+}
+
+struct BwdPlan {
+    int32_t* users = nullptr;
+    int32_t* segs = nullptr;
+    int32_t* reds = nullptr;
+    int32_t nseg = 0, nred = 0, nslots = 0;
+};
+std::map<std::tuple<int, int64_t, int32_t, int32_t>, BwdPlan> g_bwd_plans;
+
+int bwd_workspace_bytes(int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t B, int32_t L,
+                        int64_t* bytes) {
+    BwdLayout lay;
+    if (!bwd_layout(n, B, L, &lay, false)) return BF1_ERR_INVALID_ARG;
+    const int64_t delta = ((int64_t)batch * Hq * n * 4 + 255) / 256 * 256;
+    const int64_t part = (int64_t)batch * Hkv * lay.nslots * 2 * 64 * 128 * 4;
+    *bytes = delta + part;
+    return BF1_OK;
+}
+
+int get_bwd_plan(int64_t n, int32_t B, int32_t L, BwdPlan* out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return BF1_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto key = std::make_tuple(dev, n, B, L);
+    auto it = g_bwd_plans.find(key);
+    if (it == g_bwd_plans.end()) {
+        BwdLayout lay;
+        if (!bwd_layout(n, B, L, &lay, true)) return BF1_ERR_INVALID_ARG;
+        BwdPlan p;
+        p.nseg = (int32_t)(lay.segs.size() / 8);
+        p.nred = (int32_t)(lay.reds.size() / 4);
+        p.nslots = lay.nslots;
+        auto up = [](const std::vector<int32_t>& v, int32_t** d) -> bool {
+            const size_t bytes = sizeof(int32_t) * (v.empty() ? 1 : v.size());
+            if (hipMalloc((void**)d, bytes) != hipSuccess) return false;
+            if (!v.empty() && hipMemcpy(*d, v.data(), sizeof(int32_t) * v.size(),
+                                        hipMemcpyHostToDevice) != hipSuccess)
+                return false;
+            return true;
+        };
+        if (!up(lay.users, &p.users) || !up(lay.segs, &p.segs) || !up(lay.reds, &p.reds)) {
+            (void)hipFree(p.users);
+            (void)hipFree(p.segs);
+            (void)hipFree(p.reds);
+            return BF1_ERR_NOMEM;
+        }
+        it = g_bwd_plans.emplace(key, p).first;
+    }
+    *out = it->second;
+    return BF1_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -111,46 +262,10 @@ int bf1_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
     if (L < 0) return BF1_ERR_INVALID_ARG;
     if (B != 64 && B != 128) return BF1_ERR_UNSUPPORTED;
     if (batch == 0 || n == 0) return BF1_OK;
-    int64_t NB, nnz;
-    if (!route_sizes(n, B, L, &NB, &nnz)) return BF1_ERR_INVALID_ARG;
     hipStream_t s = (hipStream_t)stream;
-
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return BF1_ERR_HIP;
     Plan plan;
-    {
-        std::lock_guard<std::mutex> lock(g_mu);
-        auto key = std::make_tuple(dev, n, B, L);
-        auto it = g_plans.find(key);
-        if (it == g_plans.end()) {
-            Plan p;
-            p.nnz = nnz;
-            if (hipMalloc((void**)&p.row_ptr, sizeof(int32_t) * (NB + 1)) != hipSuccess)
-                return BF1_ERR_NOMEM;
-            if (hipMalloc((void**)&p.col_idx, sizeof(int32_t) * (nnz > 0 ? nnz : 1)) != hipSuccess) {
-                (void)hipFree(p.row_ptr);
-                return BF1_ERR_NOMEM;
-            }
-            if (hipEventCreateWithFlags(&p.ready, hipEventDisableTiming) != hipSuccess) {
-                (void)hipFree(p.row_ptr);
-                (void)hipFree(p.col_idx);
-                return BF1_ERR_HIP;
-            }
-            hipError_t e = bf1::launch_plan((int32_t)NB, L, p.row_ptr, p.col_idx, s);
-            if (e == hipSuccess) e = hipEventRecord(p.ready, s);
-            if (e != hipSuccess) {
-                (void)hipFree(p.row_ptr);
-                (void)hipFree(p.col_idx);
-                (void)hipEventDestroy(p.ready);
-                return BF1_ERR_HIP;
-            }
-            it = g_plans.emplace(key, p).first;
-        }
-        plan = it->second;
-    }
-    // The plan may have been built on another stream: order this one after it.
-    if (hipStreamWaitEvent(s, plan.ready, 0) != hipSuccess) return BF1_ERR_HIP;
-
+    st = get_plan(n, B, L, s, &plan);
+    if (st != BF1_OK) return st;
     bf1::AttnArgs a{Q, K, V, O, LSE, plan.row_ptr, plan.col_idx, plan.nnz,
                     batch, n, Hq, Hkv, head_dim, B, false};
     return run_attn(a, s);
@@ -181,6 +296,65 @@ int bf1_dense_causal_fwd(const void* Q, const void* K, const void* V, void* O, f
     return run_attn(a, (hipStream_t)stream);
 }
 
+int bf1_plan_transposed(int64_t n, int32_t B, int32_t L, int32_t* row_ptr, int32_t* col_idx,
+                        int64_t col_capacity) {
+    if (n < 0 || B < 1 || L < 0 || col_capacity < 0 || !row_ptr) return BF1_ERR_INVALID_ARG;
+    int64_t NB, nnz;
+    if (!route_sizes(n, B, L, &NB, &nnz)) return BF1_ERR_INVALID_ARG;
+    if (nnz > 0 && !col_idx) return BF1_ERR_INVALID_ARG;
+    if (col_capacity < nnz) return BF1_ERR_BUFFER_TOO_SMALL;
+    int64_t e = 0;
+    for (int64_t i = 0; i < NB; ++i) {
+        row_ptr[i] = (int32_t)e;
+        e += bf1::route_users(NB, L, i, col_idx ? col_idx + e : nullptr);
+    }
+    row_ptr[NB] = (int32_t)e;
+    return e == nnz ? BF1_OK : BF1_ERR_INVALID_ARG;
+}
+
+int bf1_attn_bwd_workspace_size(int32_t batch, int64_t n, int32_t Hq, int32_t Hkv,
+                                int32_t head_dim, int32_t B, int32_t L, int64_t* bytes) {
+    if (!bytes) return BF1_ERR_INVALID_ARG;
+    int st = check_attn(nullptr, nullptr, nullptr, nullptr, nullptr, 0, n, Hq, Hkv, head_dim);
+    if (st != BF1_OK) return st;
+    if (batch < 0 || L < 0) return BF1_ERR_INVALID_ARG;
+    if (head_dim != 128 || (B != 64 && B != 128) || (Hq / Hkv) * B < 128) return BF1_ERR_UNSUPPORTED;
+    return bwd_workspace_bytes(batch, n, Hq, Hkv, B, L, bytes);
+}
+
+int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                 const float* LSE, float* dQ, float* dK, float* dV, int32_t batch, int64_t n,
+                 int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t B, int32_t L, void* workspace,
+                 int64_t workspace_bytes, void* stream) {
+    int st = check_attn(Q, K, V, const_cast<void*>(O), nullptr, batch, n, Hq, Hkv, head_dim);
+    if (st != BF1_OK) return st;
+    if (L < 0 || workspace_bytes < 0) return BF1_ERR_INVALID_ARG;
+    if (head_dim != 128 || (B != 64 && B != 128) || (Hq / Hkv) * B < 128) return BF1_ERR_UNSUPPORTED;
+    if (batch == 0 || n == 0) return BF1_OK;
+    if (!dO || !LSE || !dQ || !dK || !dV || !workspace) return BF1_ERR_INVALID_ARG;
+    if (!aligned(dO, 16) || !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) ||
+        !aligned(LSE, 4) || !aligned(workspace, 256))
+        return BF1_ERR_INVALID_ARG;
+    int64_t need = 0;
+    st = bwd_workspace_bytes(batch, n, Hq, Hkv, B, L, &need);
+    if (st != BF1_OK) return st;
+    if (workspace_bytes < need) return BF1_ERR_BUFFER_TOO_SMALL;
+    hipStream_t s = (hipStream_t)stream;
+    Plan plan;
+    st = get_plan(n, B, L, s, &plan);
+    if (st != BF1_OK) return st;
+    BwdPlan bp;
+    st = get_bwd_plan(n, B, L, &bp);
+    if (st != BF1_OK) return st;
+    const int64_t delta_bytes = ((int64_t)batch * Hq * n * 4 + 255) / 256 * 256;
+    float* delta = (float*)workspace;
+    float* part = (float*)((char*)workspace + delta_bytes);
+    bf1::BwdArgs a{Q, K, V, O, dO, LSE, dQ, dK, dV, delta, part,
+                   plan.row_ptr, plan.col_idx, plan.nnz, bp.users, bp.segs, bp.nseg,
+                   bp.reds, bp.nred, bp.nslots, batch, n, Hq, Hkv, B};
+    return status_of(bf1::launch_backward(a, s));
+}
+
 void bf1_release_plans(void) {
     std::lock_guard<std::mutex> lock(g_mu);
     for (auto& kv : g_plans) {
@@ -190,6 +364,13 @@ void bf1_release_plans(void) {
         (void)hipEventDestroy(kv.second.ready);
     }
     g_plans.clear();
+    if (!g_bwd_plans.empty()) (void)hipDeviceSynchronize();
+    for (auto& kv : g_bwd_plans) {
+        (void)hipFree(kv.second.users);
+        (void)hipFree(kv.second.segs);
+        (void)hipFree(kv.second.reds);
+    }
+    g_bwd_plans.clear();
 }
 
 }  // extern "C"

@@ -1,0 +1,544 @@
+// BF1 causal dyadic block-sparse attention: backward kernels for gfx950
+// (head_dim 128).  Gradients of O = softmax_mask(c Q K^T) V with respect to Q,
+// K and V for an upstream gradient dO, on the route of the paper's §3.1
+// (Eq. 1), with P recomputed from the forward's log-sum-exp:
+//     P = exp(c S - LSE),  D = rowsum(dO * O),  dP = dO V^T,  dS = P * (dP - D),
+//     dQ = c dS K,  dK = c dS^T Q,  dV = P^T dO   (summed over a GQA group).
+//
+// Kernels:
+//  * bwd_dq_kernel   -- one workgroup per (batch, kv-head, query block, row
+//    chunk), walking the forward route like the forward kernel; computes D
+//    for its rows (written for the next kernel) and dQ.
+//  * bwd_dkdv_kernel -- one workgroup per (batch, kv-head, 64-key tile,
+//    segment of the tile's query-block list), walking the TRANSPOSED route
+//    (the query blocks that select the key block); accumulates dK and dV in
+//    registers.  Key block 0 is selected by every query block, so long lists
+//    are cut into segments whose partial sums go to a workspace.
+//  * bwd_reduce_kernel -- sums the segment partials of such tiles in a fixed
+//    order (deterministic) into dK and dV.
+//
+// Tiles in LDS keep the natural [row][d] order in 16-byte chunks; chunk c of
+// row r sits at c ^ bswz(r), bswz(r) = 4 (r mod 4) + (r/4 mod 4).  This one
+// layout is conflict-free for both ways the backward reads a tile: 16 bytes
+// of one row per lane (an MFMA operand with k along d) and the LDS transpose
+// load (an operand with k along the rows).  Matrix-core layouts follow the
+// forward (v_mfma_f32_32x32x16_bf16; accumulator lane l, register r holds
+// row 8(r/4) + 4(l/32) + r%4, column l%32).
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "bf1_device.h"
+#include "bf1_kernels.h"
+
+namespace bf1 {
+namespace {
+
+constexpr int BD = 128;          // head_dim of the backward kernels
+constexpr int BRB = BD * 2;      // bytes per bf16 row
+constexpr int BTILE = KT * BRB;  // bytes per 64-row tile (16 KB)
+constexpr int BKS = BD / 16;     // MFMA k-steps along d
+constexpr int BDT = BD / 32;     // 32-wide d tiles
+
+__device__ __forceinline__ int bswz(int row) { return 4 * (row & 3) + ((row >> 2) & 3); }
+
+// Byte offset, inside a tile, of the 16 bytes lane `lane` moves in the direct
+// load of 1 KB segment `seg` (rows 4 seg .. 4 seg + 3, lane order = physical).
+__device__ __forceinline__ uint32_t seg_off(int seg, int lane) {
+    const int row = seg * 4 + (lane >> 4), pc = lane & 15;
+    return (uint32_t)(row * BRB + ((pc ^ bswz(row)) << 4));
+}
+// Row-wise operand read: 16 bytes of `row`, logical chunk c.
+__device__ __forceinline__ int rw_off(int row, int c) { return row * BRB + ((c ^ bswz(row)) << 4); }
+// Transpose-read base of lane `lane` for d-tile dt, second read of a pair h2
+// (rows +8); a 16-row group g adds 16 g rows (bswz is unchanged by it).
+__device__ __forceinline__ int tr_off(int lane, int dt, int h2) {
+    const int gq = lane >> 4, kk = lane & 15;
+    const int row = 4 * (gq >> 1) + (kk >> 2) + 8 * h2;
+    const int lb = 32 * (2 * dt + (gq & 1)) + 8 * (kk & 3);
+    return row * BRB + (((lb >> 4) ^ bswz(row)) << 4) + (lb & 15);
+}
+
+__device__ __forceinline__ float dot_bf16x8(u32x4 a, u32x4 b) {
+    const bf16x8 x = __builtin_bit_cast(bf16x8, a), y = __builtin_bit_cast(bf16x8, b);
+    float s = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s = fmaf((float)x[e], (float)y[e], s);
+    return s;
+}
+
+// ---------------------------------------------------------------------------
+// dQ (and D)
+// ---------------------------------------------------------------------------
+// Workgroup = 4 waves x 32 stacked query rows (like the forward); per tile of
+// 64 keys each wave computes S^T = K Q^T and dP^T = V dO^T (A operands: rows
+// of the K and V tiles; B operands: this lane's query row of Q and dO, held in
+// registers), P^T = exp2(c log2e S^T - log2e LSE), dS^T = P^T (dP^T - D), and
+// dQ^T += K^T dS^T (A operand: transpose reads of the K tile; B: dS^T packed
+// to bf16 from the lane's own registers).  Double-buffered K/V tiles, one
+// barrier per tile.
+template <int G, int BW, bool DENSE>
+__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
+    const __bf16* __restrict__ O, const __bf16* __restrict__ dO, const float* __restrict__ LSE,
+    float* __restrict__ dQ, float* __restrict__ Delta, const int32_t* __restrict__ row_ptr,
+    const int32_t* __restrict__ col_idx, int64_t nnz, int32_t n, int32_t NB, int32_t batch_hkv,
+    int32_t Hkv, float c_log2, float scale) {
+    constexpr int NW = 4, ROWS = 128;
+    constexpr int NCHUNK = (G * BW) / ROWS;
+    constexpr int NSUB = BW / KT;
+    constexpr int SPW = (BTILE / 1024) / NW;  // K (or V) segments per wave per tile
+    static_assert(NCHUNK * ROWS == G * BW, "rows must tile the stacked group");
+
+    __shared__ u32x4 kt_s[2][BTILE / 16];
+    __shared__ u32x4 vt_s[2][BTILE / 16];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int col = lane & 31;
+    const int half = lane >> 5;
+
+    const int32_t x = blockIdx.x;
+    const int chunk = x % NCHUNK;
+    const int32_t y = x / NCHUNK;
+    const int32_t bh = y % batch_hkv;
+    const int32_t j = NB - 1 - y / batch_hkv;
+    const int32_t beta = bh / Hkv;
+    const int32_t g = bh % Hkv;
+    const int Hq = Hkv * G;
+
+    const int srow = chunk * ROWS + wave * 32;
+    const int head = g * G + srow / BW;
+    const int qin = srow % BW + col;  // query position inside block j
+    const int32_t qpos = j * BW + qin;
+    const bool qvalid = qpos < n;
+    const int64_t qrow = ((int64_t)beta * Hq + head) * (int64_t)n + qpos;
+
+    // ---- Q, dO rows (B operands) and D = dO . O --------------------------------
+    bf16x8 qf[BKS], dof[BKS];
+    float dpart = 0.f;
+    {
+        const u32x4* qs = reinterpret_cast<const u32x4*>(Q + qrow * BD);
+        const u32x4* ds = reinterpret_cast<const u32x4*>(dO + qrow * BD);
+        const u32x4* os = reinterpret_cast<const u32x4*>(O + qrow * BD);
+#pragma unroll
+        for (int s = 0; s < BKS; ++s) {
+            u32x4 wq = {0u, 0u, 0u, 0u}, wd = wq, wo = wq;
+            if (qvalid) {
+                wq = qs[2 * s + half];
+                wd = ds[2 * s + half];
+                wo = os[2 * s + half];
+            }
+            qf[s] = __builtin_bit_cast(bf16x8, wq);
+            dof[s] = __builtin_bit_cast(bf16x8, wd);
+            dpart += dot_bf16x8(wd, wo);
+        }
+    }
+    const float Dq = pair_sum(dpart);  // the two lane halves hold the two halves of d
+    if (qvalid && half == 0) Delta[qrow] = Dq;
+    const float lse2 = qvalid ? LSE[qrow] * LOG2E : INFINITY;  // rows past n: P = 0
+
+    // ---- route walk (as in the forward) -------------------------------------------
+    int32_t pos_end, cur_p;
+    if (DENSE) {
+        cur_p = 0;
+        pos_end = j + 1;
+    } else {
+        int64_t e0 = row_ptr[j], e1 = row_ptr[j + 1];
+        e0 = e0 < 0 ? 0 : (e0 > nnz ? nnz : e0);
+        e1 = e1 < e0 ? e0 : (e1 > nnz ? nnz : e1);
+        cur_p = (int32_t)e0;
+        pos_end = (int32_t)e1;
+    }
+    int cur_u = 0;
+    auto next_tile = [&](int32_t& ti, int& tu) -> bool {
+        while (cur_p < pos_end) {
+            const int32_t i = DENSE ? cur_p : col_idx[cur_p];
+            if (i >= 0 && i <= j) {
+                for (; cur_u < NSUB; ++cur_u)
+                    if (i * BW + cur_u * KT < n) {
+                        ti = i;
+                        tu = cur_u++;
+                        if (cur_u >= NSUB) {
+                            ++cur_p;
+                            cur_u = 0;
+                        }
+                        return true;
+                    }
+            }
+            ++cur_p;
+            cur_u = 0;
+        }
+        return false;
+    };
+
+    const uint32_t head_bytes = (uint32_t)n * BRB;
+    const __amdgpu_buffer_rsrc_t k_rsrc =
+        head_rsrc(K + ((int64_t)beta * Hkv + g) * (int64_t)n * BD, head_bytes);
+    const __amdgpu_buffer_rsrc_t v_rsrc =
+        head_rsrc(V + ((int64_t)beta * Hkv + g) * (int64_t)n * BD, head_bytes);
+    auto stage = [&](int buf, int32_t ti, int tu) {
+        const uint32_t soff = (uint32_t)(ti * BW + tu * KT) * BRB;
+#pragma unroll
+        for (int it = 0; it < SPW; ++it) {
+            const int seg = it * NW + wave;
+            load_lds_async<16>(k_rsrc, &kt_s[buf][seg * 64], seg_off(seg, lane), soff);
+            load_lds_async<16>(v_rsrc, &vt_s[buf][seg * 64], seg_off(seg, lane), soff);
+        }
+    };
+
+    f32x16 acc[BDT];
+#pragma unroll
+    for (int t = 0; t < BDT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
+
+    int32_t ti = 0, tn = 0;
+    int tu = 0, tnu = 0;
+    bool have = next_tile(ti, tu);
+    if (have) stage(0, ti, tu);
+    __builtin_amdgcn_s_waitcnt(VMCNT0);
+    __syncthreads();
+    int buf = 0;
+    const f32x16 zero = {};
+    while (have) {
+        const bool hn = next_tile(tn, tnu);
+        if (hn) stage(buf ^ 1, tn, tnu);
+
+        const char* kb = reinterpret_cast<const char*>(&kt_s[buf][0]);
+        const char* vb = reinterpret_cast<const char*>(&vt_s[buf][0]);
+        f32x16 st[2], dpt[2];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int ks = 0; ks < BKS; ++ks) {
+                const int o = rw_off(32 * kt + col, 2 * ks + half);
+                const u32x4 ka = *reinterpret_cast<const u32x4*>(kb + o);
+                const u32x4 va = *reinterpret_cast<const u32x4*>(vb + o);
+                st[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, ka), qf[ks], ks == 0 ? zero : st[kt], 0, 0, 0);
+                dpt[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, va), dof[ks], ks == 0 ? zero : dpt[kt], 0, 0, 0);
+            }
+        // dS^T = P^T (dP^T - D), packed as the B operands of K^T dS^T
+        bf16x8 db[4];
+        const bool self = ti == j;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+            f32x8 v8;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int kp = tu * KT + 32 * kt + 8 * (r >> 2) + 4 * half + (r & 3);
+                float p = __builtin_amdgcn_exp2f(fmaf(st[kt][r], c_log2, -lse2));
+                if (self && kp > qin) p = 0.f;
+                v8[r & 7] = p * (dpt[kt][r] - Dq);
+                if ((r & 7) == 7) db[2 * kt + (r >> 3)] = __builtin_convertvector(v8, bf16x8);
+            }
+        }
+        const uint32_t kl = lds_addr(kb);
+#pragma unroll
+        for (int dt = 0; dt < BDT; ++dt) {
+            const uint32_t a0 = kl + tr_off(lane, dt, 0), a1 = kl + tr_off(lane, dt, 1);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const u32x2 lo = lds_read_tr16(a0 + 16 * t * BRB);
+                const u32x2 hi = lds_read_tr16(a1 + 16 * t * BRB);
+                const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
+                acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w),
+                                                                  db[t], acc[dt], 0, 0, 0);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(VMCNT0);  // this wave's loads of the next tile have landed
+        __syncthreads();                      // ... and every other wave's; this tile is free
+        ti = tn;
+        tu = tnu;
+        have = hn;
+        buf ^= 1;
+    }
+    __builtin_amdgcn_s_waitcnt(VMCNT0);
+
+    // ---- dQ = c dS K (rows past n are not stored) -----------------------------------
+    if (!qvalid) return;
+    float* drow = dQ + qrow * BD;
+#pragma unroll
+    for (int dt = 0; dt < BDT; ++dt)
+#pragma unroll
+        for (int gq4 = 0; gq4 < 4; ++gq4) {
+            f32x4 v4;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) v4[c] = acc[dt][4 * gq4 + c] * scale;
+            *reinterpret_cast<f32x4*>(drow + 32 * dt + 8 * gq4 + 4 * half) = v4;
+        }
+}
+
+// ---------------------------------------------------------------------------
+// dK, dV
+// ---------------------------------------------------------------------------
+// Workgroup = 2 waves; wave w owns keys 32 w .. 32 w + 31 of one 64-key tile
+// (block i, sub-tile u) and holds their K^T and V^T as MFMA B operands in
+// registers.  It walks query tiles (64 rows of one q-head of a query block j
+// that selects block i), staged in LDS: Q and dO rows, LSE and D.  Per 32-row
+// half of a query tile:
+//   S = Q K^T, dP = dO V^T          (A: row-wise reads of the Q / dO tiles)
+//   P = exp2(c log2e S - log2e LSE), dS = P (dP - D)   (lane = key column)
+//   dV += P^T dO, dK += dS^T Q      (A: P / dS packed from the lane's own
+//                                    registers; B: transpose reads of dO / Q)
+// A segment descriptor (int32 x 8): key block, sub-tile, first entry of its
+// query-block list in the transposed table, entry count, partial slot (-1:
+// write dK/dV directly).
+template <int G, int BW>
+__global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
+    const __bf16* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ Delta,
+    float* __restrict__ dK, float* __restrict__ dV, float* __restrict__ part,
+    const int32_t* __restrict__ segs, const int32_t* __restrict__ users, int32_t nslots,
+    int32_t n, int32_t batch_hkv, int32_t Hkv, float c_log2, float scale) {
+    constexpr int NW = 2;
+    constexpr int NSUB = BW / KT;
+    constexpr int SPW = (BTILE / 1024) / NW;  // Q (or dO) segments per wave per tile
+
+    __shared__ u32x4 q_s[2][BTILE / 16];
+    __shared__ u32x4 o_s[2][BTILE / 16];
+    __shared__ float lse_s[2][KT];
+    __shared__ float del_s[2][KT];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int col = lane & 31;
+    const int half = lane >> 5;
+
+    const int32_t x = blockIdx.x;
+    const int32_t bh = x % batch_hkv;
+    const int32_t* sd = segs + 8 * (x / batch_hkv);
+    const int32_t i = sd[0];
+    const int u = sd[1];
+    const int32_t uoff = sd[2];
+    const int32_t ucnt = sd[3];
+    const int32_t slot = sd[4];
+    const int32_t beta = bh / Hkv;
+    const int32_t g = bh % Hkv;
+    const int Hq = Hkv * G;
+
+    const int kin = u * KT + 32 * wave + col;  // key position inside block i of this lane's column
+    const int32_t kpos = i * BW + kin;
+    const int64_t kvrow0 = ((int64_t)beta * Hkv + g) * (int64_t)n;
+
+    // ---- K^T and V^T of this wave's 32 keys (B operands), zero past n ---------------
+    bf16x8 kf[BKS], vf[BKS];
+    {
+        const u32x4* ks = reinterpret_cast<const u32x4*>(K + (kvrow0 + kpos) * BD);
+        const u32x4* vs = reinterpret_cast<const u32x4*>(V + (kvrow0 + kpos) * BD);
+#pragma unroll
+        for (int s = 0; s < BKS; ++s) {
+            u32x4 wk = {0u, 0u, 0u, 0u}, wv = wk;
+            if (kpos < n) {
+                wk = ks[2 * s + half];
+                wv = vs[2 * s + half];
+            }
+            kf[s] = __builtin_bit_cast(bf16x8, wk);
+            vf[s] = __builtin_bit_cast(bf16x8, wv);
+        }
+    }
+
+    // Query tile t of this segment: entry t / (G NSUB) of the list, q-head
+    // t / NSUB % G of the group, sub-tile t % NSUB of the query block.
+    const int32_t ntiles = ucnt * G * NSUB;
+    auto stage = [&](int buf, int32_t t) {
+        const int32_t jq = users[uoff + t / (G * NSUB)];
+        const int h = g * G + (t / NSUB) % G;
+        const int32_t row0 = jq * BW + (t % NSUB) * KT;
+        const int64_t qr0 = ((int64_t)beta * Hq + h) * (int64_t)n;
+        const __amdgpu_buffer_rsrc_t qr = head_rsrc(Q + qr0 * BD, (uint32_t)n * BRB);
+        const __amdgpu_buffer_rsrc_t orr = head_rsrc(dO + qr0 * BD, (uint32_t)n * BRB);
+        const uint32_t soff = (uint32_t)row0 * BRB;
+#pragma unroll
+        for (int it = 0; it < SPW; ++it) {
+            const int seg = it * NW + wave;
+            load_lds_async<16>(qr, &q_s[buf][seg * 64], seg_off(seg, lane), soff);
+            load_lds_async<16>(orr, &o_s[buf][seg * 64], seg_off(seg, lane), soff);
+        }
+        // 64 rows of LSE (wave 0) or D (wave 1), 4 bytes per lane
+        const float* src = (wave == 0 ? LSE : Delta) + qr0;
+        float* dst = wave == 0 ? &lse_s[buf][0] : &del_s[buf][0];
+        load_lds_async<4>(head_rsrc(src, (uint32_t)n * 4), dst, (uint32_t)lane * 4, (uint32_t)row0 * 4);
+    };
+    auto tile_query_block = [&](int32_t t) -> int32_t { return users[uoff + t / (G * NSUB)]; };
+
+    f32x16 dk[BDT], dv[BDT];
+#pragma unroll
+    for (int t = 0; t < BDT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dk[t][r] = dv[t][r] = 0.f;
+
+    if (ntiles > 0) stage(0, 0);
+    __builtin_amdgcn_s_waitcnt(VMCNT0);
+    __syncthreads();
+    const f32x16 zero = {};
+    for (int32_t t = 0, buf = 0; t < ntiles; ++t, buf ^= 1) {
+        if (t + 1 < ntiles) stage(buf ^ 1, t + 1);
+        const int32_t jq = tile_query_block(t);
+        const bool self = jq == i;
+        const int qsub = (t % NSUB) * KT;  // query position of tile row 0 inside block jq
+        const char* qb = reinterpret_cast<const char*>(&q_s[buf][0]);
+        const char* ob = reinterpret_cast<const char*>(&o_s[buf][0]);
+        const uint32_t ql = lds_addr(qb), ol = lds_addr(ob);
+#pragma unroll
+        for (int rh = 0; rh < 2; ++rh) {
+            f32x16 s, dp;
+#pragma unroll
+            for (int ks = 0; ks < BKS; ++ks) {
+                const int o = rw_off(32 * rh + col, 2 * ks + half);
+                const u32x4 qa = *reinterpret_cast<const u32x4*>(qb + o);
+                const u32x4 oa = *reinterpret_cast<const u32x4*>(ob + o);
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, qa), kf[ks],
+                                                            ks == 0 ? zero : s, 0, 0, 0);
+                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, oa), vf[ks],
+                                                             ks == 0 ? zero : dp, 0, 0, 0);
+            }
+            // rows of this lane: 32 rh + 8 g4 + 4 half + c
+            bf16x8 pa[2], da[2];
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+                const int rbase = 32 * rh + 8 * g4 + 4 * half;
+                const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse_s[buf][rbase]);
+                const f32x4 d4 = *reinterpret_cast<const f32x4*>(&del_s[buf][rbase]);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int r = 4 * g4 + c;
+                    float p = __builtin_amdgcn_exp2f(fmaf(s[r], c_log2, -l4[c] * LOG2E));
+                    if (self && kin > qsub + rbase + c) p = 0.f;
+                    const float ds = p * (dp[r] - d4[c]);
+                    pa[r >> 3][r & 7] = (__bf16)p;
+                    da[r >> 3][r & 7] = (__bf16)ds;
+                }
+            }
+#pragma unroll
+            for (int dt = 0; dt < BDT; ++dt) {
+#pragma unroll
+                for (int m = 0; m < 2; ++m) {
+                    const int go = 16 * (2 * rh + m) * BRB;
+                    const u32x2 olo = lds_read_tr16(ol + tr_off(lane, dt, 0) + go);
+                    const u32x2 ohi = lds_read_tr16(ol + tr_off(lane, dt, 1) + go);
+                    const u32x2 qlo = lds_read_tr16(ql + tr_off(lane, dt, 0) + go);
+                    const u32x2 qhi = lds_read_tr16(ql + tr_off(lane, dt, 1) + go);
+                    const u32x4 wo = {olo[0], olo[1], ohi[0], ohi[1]};
+                    const u32x4 wq = {qlo[0], qlo[1], qhi[0], qhi[1]};
+                    dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa[m], __builtin_bit_cast(bf16x8, wo),
+                                                                     dv[dt], 0, 0, 0);
+                    dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da[m], __builtin_bit_cast(bf16x8, wq),
+                                                                     dk[dt], 0, 0, 0);
+                }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(VMCNT0);  // this wave's loads of the next tile have landed
+        __syncthreads();                      // ... and the other wave's; this tile is free
+    }
+    __builtin_amdgcn_s_waitcnt(VMCNT0);
+
+    // ---- store: lane holds d column 32 dt + col, keys 8(r/4) + 4 half + r%4 ---------
+    // Directly into dK/dV (keys past n skipped) or into the segment's partial slot.
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int key = 32 * wave + 8 * (r >> 2) + 4 * half + (r & 3);  // inside the 64-key tile
+        if (slot < 0) {
+            const int32_t kp = i * BW + u * KT + key;
+            if (kp >= n) continue;
+            float* krow = dK + (kvrow0 + kp) * BD;
+            float* vrow = dV + (kvrow0 + kp) * BD;
+#pragma unroll
+            for (int dt = 0; dt < BDT; ++dt) {
+                krow[32 * dt + col] = dk[dt][r] * scale;
+                vrow[32 * dt + col] = dv[dt][r];
+            }
+        } else {
+            float* pk = part + (((int64_t)bh * nslots + slot) * 2) * (KT * BD) + key * BD;
+            float* pv = pk + KT * BD;
+#pragma unroll
+            for (int dt = 0; dt < BDT; ++dt) {
+                pk[32 * dt + col] = dk[dt][r] * scale;
+                pv[32 * dt + col] = dv[dt][r];
+            }
+        }
+    }
+}
+
+// Sum of the partial slots of split key tiles: reduce descriptor (int32 x 4) =
+// key block, sub-tile, first slot, slot count.  Fixed summation order.
+template <int BW>
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(
+    float* __restrict__ dK, float* __restrict__ dV, const float* __restrict__ part,
+    const int32_t* __restrict__ reds, int32_t nslots, int32_t n, int32_t batch_hkv) {
+    const int32_t x = blockIdx.x;
+    const int32_t bh = x % batch_hkv;
+    const int32_t* rd = reds + 4 * (x / batch_hkv);
+    const int32_t i = rd[0], u = rd[1], s0 = rd[2], ns = rd[3];
+    const int64_t kvrow0 = (int64_t)bh * n;
+    for (int e = threadIdx.x; e < KT * BD; e += blockDim.x) {
+        const int key = e / BD, d = e % BD;
+        const int32_t kp = i * BW + u * KT + key;
+        if (kp >= n) continue;
+        float sk = 0.f, sv = 0.f;
+        for (int32_t s = 0; s < ns; ++s) {
+            const float* pk = part + (((int64_t)bh * nslots + s0 + s) * 2) * (KT * BD);
+            sk += pk[e];
+            sv += pk[KT * BD + e];
+        }
+        dK[(kvrow0 + kp) * BD + d] = sk;
+        dV[(kvrow0 + kp) * BD + d] = sv;
+    }
+}
+
+template <int G, int BW>
+hipError_t launch_bwd_g(const BwdArgs& a, hipStream_t stream) {
+    constexpr int NCHUNK = (G * BW) / 128;
+    const int32_t NB = (int32_t)((a.n + BW - 1) / BW);
+    const int32_t bhk = a.batch * a.Hkv;
+    const int64_t items = (int64_t)NB * bhk * NCHUNK;
+    if (items > 0x7fffffff || (int64_t)a.nseg * bhk > 0x7fffffff || (int64_t)a.nred * bhk > 0x7fffffff)
+        return hipErrorInvalidValue;
+    const float scale = 1.0f / sqrtf((float)BD);
+    const float c_log2 = scale * LOG2E;
+    hipLaunchKernelGGL((bwd_dq_kernel<G, BW, false>), dim3((unsigned)items), dim3(256), 0, stream,
+                       (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, (const __bf16*)a.O,
+                       (const __bf16*)a.dO, a.LSE, a.dQ, a.delta, a.row_ptr, a.col_idx, a.nnz,
+                       (int32_t)a.n, NB, bhk, a.Hkv, c_log2, scale);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (a.nseg > 0) {
+        hipLaunchKernelGGL((bwd_dkdv_kernel<G, BW>), dim3((unsigned)(a.nseg * bhk)), dim3(128), 0,
+                           stream, (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
+                           (const __bf16*)a.dO, a.LSE, a.delta, a.dK, a.dV, a.part, a.segs,
+                           a.users, a.nslots, (int32_t)a.n, bhk, a.Hkv, c_log2, scale);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (a.nred > 0) {
+        hipLaunchKernelGGL((bwd_reduce_kernel<BW>), dim3((unsigned)(a.nred * bhk)), dim3(256), 0,
+                           stream, a.dK, a.dV, a.part, a.reds, a.nslots, (int32_t)a.n, bhk);
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+template <int BW>
+hipError_t launch_bwd_b(const BwdArgs& a, hipStream_t s) {
+    switch (a.Hq / a.Hkv) {
+        case 1:
+            if constexpr (BW >= 128) return launch_bwd_g<1, BW>(a, s);
+            return hipErrorInvalidValue;  // G * B < 128: rejected by the interface
+        case 2: return launch_bwd_g<2, BW>(a, s);
+        case 4: return launch_bwd_g<4, BW>(a, s);
+        default: return launch_bwd_g<8, BW>(a, s);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_backward(const BwdArgs& a, hipStream_t stream) {
+    if (a.B == 64) return launch_bwd_b<64>(a, stream);
+    return launch_bwd_b<128>(a, stream);
+}
+
+}  // namespace bf1

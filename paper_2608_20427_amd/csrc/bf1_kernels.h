@@ -24,6 +24,37 @@ struct AttnArgs {
     bool dense;             // implicit route {0..j} over 64-token blocks
 };
 
+// Backward (head_dim 128; G * B >= 128).  All pointers are device memory.
+struct BwdArgs {
+    const void* Q;
+    const void* K;
+    const void* V;
+    const void* O;
+    const void* dO;
+    const float* LSE;
+    float* dQ;               // [batch, Hq, n, 128] fp32
+    float* dK;               // [batch, Hkv, n, 128] fp32
+    float* dV;
+    float* delta;            // workspace: [batch, Hq, n] fp32 (D = rowsum(dO * O))
+    float* part;             // workspace: [batch * Hkv, nslots, 2, 64, 128] fp32
+    const int32_t* row_ptr;  // forward route (CSR)
+    const int32_t* col_idx;
+    int64_t nnz;
+    const int32_t* users;    // transposed route entries (query blocks per key block)
+    const int32_t* segs;     // [nseg][8]: key block, sub-tile, first entry, count, slot
+    int32_t nseg;
+    const int32_t* reds;     // [nred][4]: key block, sub-tile, first slot, slot count
+    int32_t nred;
+    int32_t nslots;
+    int32_t batch;
+    int64_t n;
+    int32_t Hq;
+    int32_t Hkv;
+    int32_t B;               // block width 64 or 128
+};
+
+hipError_t launch_backward(const BwdArgs& a, hipStream_t stream);
+
 // Route planner: row_ptr[0..NB], col_idx[0..nnz) on `stream`.
 hipError_t launch_plan(int32_t NB, int32_t L, int32_t* row_ptr, int32_t* col_idx,
                        hipStream_t stream);

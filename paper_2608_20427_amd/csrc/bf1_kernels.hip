@@ -31,27 +31,15 @@
 
 #include <type_traits>
 
+#include "bf1_device.h"
 #include "bf1_kernels.h"
 #include "bf1_route.h"
 
 namespace bf1 {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-constexpr int KT = 64;  // keys per LDS tile
-constexpr float LOG2E = 1.4426950408889634f;
-constexpr float LN2 = 0.6931471805599453f;
 constexpr float RESCALE_LOG2 = 8.0f;  // lazy-rescale threshold (log2 units)
 constexpr int KPF = 3;                // K operand reads in flight ahead of the score MFMAs
-constexpr int VMCNT0 = 0x0F70;        // s_waitcnt vmcnt(0) (expcnt, lgkmcnt unconstrained)
 
 // ---------------------------------------------------------------------------
 // Route planner
@@ -121,15 +109,6 @@ struct TileSmem {
     u32x4 v[2][KT * D / 8];
 };
 
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-typedef __attribute__((address_space(3))) void lds_void;
-
-// LDS address (byte offset in the workgroup's LDS) of a shared-memory pointer.
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    return (uint32_t)(uintptr_t)(const lds_void*)(p);
-}
-
 // Eight 64-bit LDS transpose reads (see the V tile layout above) at constant
 // offsets O0 + k * STEP from one lane address, followed by the wait for them,
 // all in ONE inline-assembly statement.  Keeping the wait inside the statement
@@ -159,33 +138,6 @@ __device__ __forceinline__ void lds_read_tr16_x8(uint32_t addr, u32x2 (&v)[8]) {
         : "v"(addr), "i"(O0), "i"(O0 + STEP), "i"(O0 + 2 * STEP), "i"(O0 + 3 * STEP),
           "i"(O0 + 4 * STEP), "i"(O0 + 5 * STEP), "i"(O0 + 6 * STEP), "i"(O0 + 7 * STEP)
         : "memory");
-}
-
-// Combine a value with the one held by the lane 32 apart (both lane halves
-// hold the same query row).  v_permlane32_swap exchanges the halves in the
-// vector ALU, with no LDS round trip; both halves get identical results.
-__device__ __forceinline__ float pair_max(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float pair_sum(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-// Buffer resource over one head's [n, D] bf16 rows: reads at byte offsets at
-// or past the end return zero, which the staging below relies on.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t head_rsrc(const void* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
-                                             0x00020000);
-}
-
-// Direct buffer -> LDS load of 16 bytes per lane into the wave's 1 KB LDS
-// segment (lane order); voff is the lane's byte offset inside the tile, soff
-// the tile's byte offset inside the head.
-__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, void* lds_segment,
-                                           uint32_t voff, uint32_t soff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds_segment, 16, voff, soff, 0, 0);
 }
 
 // ---------------------------------------------------------------------------

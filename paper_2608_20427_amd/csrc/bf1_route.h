@@ -75,4 +75,30 @@ inline int64_t route_selected_pairs(int64_t n, int64_t b, int64_t L) {
            m * (m + 1) / 2;
 }
 
+
+// Query blocks that select key block i (the route transposed), ascending,
+// written to out (may be null); returns their number.  Key block 0 is the
+// global block of every query block; any other block i is selected by itself,
+// its L local successors i+1..i+L and the blocks i + 2^r with r >= 2 and
+// 2^r > L (smaller dyadic offsets land on the local successors), all clipped
+// to [0, NB).  Locals precede dyadics, so the list comes out sorted.
+inline int64_t route_users(int64_t NB, int64_t L, int64_t i, int32_t* out) {
+    int64_t c = 0;
+    if (i == 0) {
+        for (int64_t jq = 0; jq < NB; ++jq)
+            if (out) out[c++] = (int32_t)jq; else ++c;
+        return c;
+    }
+    for (int64_t jq = i; jq <= i + L && jq < NB; ++jq)
+        if (out) out[c++] = (int32_t)jq; else ++c;
+    for (int64_t r = 2; r < 62; ++r) {
+        const int64_t off = int64_t(1) << r;
+        if (i + off >= NB) break;
+        if (off > L) {
+            if (out) out[c++] = (int32_t)(i + off); else ++c;
+        }
+    }
+    return c;
+}
+
 }  // namespace bf1

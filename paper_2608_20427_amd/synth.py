@@ -94,6 +94,16 @@ def make_qkv(w, device="cpu"):
     return tq, tk, tv
 
 
+def make_grad_out(w, device="cpu"):
+    """Upstream gradient dO for workload ``w`` (bf16, Q's shape): standard
+    normal from its own seeded stream (PCG64 of the workload seed, stream 1),
+    so that Q, K, V are the same with or without it."""
+    rng = np.random.Generator(np.random.PCG64([w.seed, 1]))
+    g = rng.standard_normal((w.batch, w.Hq, w.n, w.d), dtype=np.float32)
+    t = torch.from_numpy(g).to(torch.bfloat16)
+    return t.to(device) if device != "cpu" else t
+
+
 def to_f64(t):
     """Exact float64 copy of a bf16 tensor as a NumPy array."""
     return t.detach().to("cpu").to(torch.float64).numpy()

@@ -103,3 +103,60 @@ def test_empty_problems_are_noops(lib):
     assert st == bf1.BF1_OK
     st = lib.bf1_dense_causal_fwd(None, None, None, None, None, 1, 0, 2, 1, 128, None)
     assert st == bf1.BF1_OK
+
+
+# ---- backward boundary ------------------------------------------------------
+
+def test_header_declares_the_backward():
+    names = declared_functions()
+    for want in ["bf1_plan_transposed", "bf1_attn_bwd_workspace_size", "bf1_attn_bwd"]:
+        assert want in names
+
+
+@pytest.mark.parametrize("n,B,L", [(1, 64, 2), (512, 64, 1), (4096, 64, 2), (32768, 64, 2),
+                                   (30001, 64, 2), (1500, 128, 2), (5000, 7, 0), (777, 64, 3),
+                                   (65536, 128, 2)])
+def test_plan_transposed_matches_oracle(lib, n, B, L):
+    rp, ci = bf1.plan_transposed(n, B, L)
+    rp_o, ci_o = orc.csr_transposed(n, B, L)
+    assert rp.tolist() == rp_o.tolist()
+    assert ci.tolist() == ci_o.tolist()
+
+
+def test_bwd_workspace_size(lib):
+    # D (batch * Hq * n fp32, 256-byte rounded) plus the partial dK/dV slots of
+    # the tiles whose query-block list is longer than one segment of 16: at
+    # 32K / b = 64 only block 0 (512 users -> 32 segments).
+    D = (1 * 16 * 32768 * 4 + 255) // 256 * 256
+    part = 1 * 8 * 32 * 2 * 64 * 128 * 4
+    assert bf1.bwd_workspace_size(1, 32768, 16, 8, 128, 64, 2) == D + part
+    # a short sequence has no split lists
+    assert bf1.bwd_workspace_size(1, 512, 2, 1, 128, 64, 1) == (2 * 512 * 4 + 255) // 256 * 256
+
+
+def test_backward_invalid_arguments_rejected_without_device(lib):
+    fake = ctypes.c_void_p(1 << 20)
+    args = [fake] * 9
+    def call(*a, ws=fake, wsb=1 << 40):
+        return lib.bf1_attn_bwd(*a, ws, wsb, None)
+    # head_dim 64 is not built for the backward
+    assert call(*args, 1, 128, 2, 1, 64, 64, 2) == bf1.BF1_ERR_UNSUPPORTED
+    # G * B < 128
+    assert call(*args, 1, 128, 2, 2, 128, 64, 2) == bf1.BF1_ERR_UNSUPPORTED
+    # missing gradient buffer / workspace, misaligned workspace, too small workspace
+    assert call(*args[:6], None, fake, fake, 1, 128, 2, 1, 128, 64, 2) == bf1.BF1_ERR_INVALID_ARG
+    assert call(*args, 1, 128, 2, 1, 128, 64, 2, ws=None) == bf1.BF1_ERR_INVALID_ARG
+    assert call(*args, 1, 128, 2, 1, 128, 64, 2, ws=ctypes.c_void_p((1 << 20) + 16)) == \
+        bf1.BF1_ERR_INVALID_ARG
+    assert call(*args, 1, 128, 2, 1, 128, 64, 2, wsb=16) == bf1.BF1_ERR_BUFFER_TOO_SMALL
+    assert call(*args, 1, 128, 2, 1, 128, 64, -1) == bf1.BF1_ERR_INVALID_ARG
+    # empty problems are no-ops
+    assert lib.bf1_attn_bwd(*([None] * 9), 0, 128, 2, 1, 128, 64, 2, None, 0, None) == bf1.BF1_OK
+    # transposed plan: capacity check
+    nb, nnz, _ = bf1.plan_size(4096, 64, 2)
+    import numpy as np
+    rp = np.zeros(nb + 1, dtype=np.int32)
+    ci = np.zeros(nnz, dtype=np.int32)
+    assert lib.bf1_plan_transposed(4096, 64, 2, rp.ctypes.data_as(ctypes.c_void_p),
+                                   ci.ctypes.data_as(ctypes.c_void_p), nnz - 1) == \
+        bf1.BF1_ERR_BUFFER_TOO_SMALL

@@ -131,3 +131,24 @@ def test_transposed_route_closed_form(NB, L):
                 r += 1
             expect = sorted(j for j in cand if j < NB)
         assert got == expect, (i, got, expect)
+
+
+def test_backward_with_exact_output_equals_exact_delta():
+    # D = rowsum(dO * O) for the exact O is the same number as rowsum(P * dP).
+    n, b, L = 150, 16, 2
+    q, k, v, w = _rand(17, 1, 4, 2, n, 6)
+    o, _ = orc.attn_gathered_fp64(q, k, v, b, L)
+    a = orc.attn_bwd_gathered_fp64(q, k, v, w, b, L)
+    c = orc.attn_bwd_gathered_fp64(q, k, v, w, b, L, o=o)
+    for x, y in zip(a, c):
+        np.testing.assert_allclose(x, y, rtol=0, atol=1e-12)
+
+
+def test_abs_terms_bound_the_gradients():
+    # |sum of terms| <= sum of |terms|, element by element.
+    n, b, L = 120, 16, 2
+    q, k, v, w = _rand(19, 1, 2, 1, n, 6)
+    g = orc.attn_bwd_gathered_fp64(q, k, v, w, b, L)
+    t = orc.attn_bwd_abs_terms_fp64(q, k, v, w, b, L)
+    for x, y in zip(g, t):
+        assert (np.abs(x) <= y + 1e-12).all()

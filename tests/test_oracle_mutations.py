@@ -134,25 +134,25 @@ def _bwd_parts(qr, kr, vr, dor, allowed, scale):
     return p, dp, delta
 
 
-def bwd_no_delta(qr, kr, vr, dor, allowed, scale):
+def bwd_no_delta(qr, kr, vr, dor, allowed, scale, delta=None):
     p, dp, _ = _bwd_parts(qr, kr, vr, dor, allowed, scale)
     ds = p * dp
     return scale * (ds @ kr), scale * (ds.T @ qr), p.T @ dor
 
 
-def bwd_sign_flip(qr, kr, vr, dor, allowed, scale):
+def bwd_sign_flip(qr, kr, vr, dor, allowed, scale, delta=None):
     p, dp, delta = _bwd_parts(qr, kr, vr, dor, allowed, scale)
     ds = p * (delta - dp)
     return scale * (ds @ kr), scale * (ds.T @ qr), p.T @ dor
 
 
-def bwd_dk_unscaled(qr, kr, vr, dor, allowed, scale):
+def bwd_dk_unscaled(qr, kr, vr, dor, allowed, scale, delta=None):
     p, dp, delta = _bwd_parts(qr, kr, vr, dor, allowed, scale)
     ds = p * (dp - delta)
     return scale * (ds @ kr), ds.T @ qr, p.T @ dor
 
 
-def bwd_dv_transposed_weights(qr, kr, vr, dor, allowed, scale):
+def bwd_dv_transposed_weights(qr, kr, vr, dor, allowed, scale, delta=None):
     p, dp, delta = _bwd_parts(qr, kr, vr, dor, allowed, scale)
     ds = p * (dp - delta)
     w = np.exp(np.where(allowed, scale * (qr @ kr.T), -np.inf))  # unnormalised weights
