@@ -465,28 +465,36 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
 }
 
 // Sum of the partial slots of split key tiles: reduce descriptor (int32 x 4) =
-// key block, sub-tile, first slot, slot count.  Fixed summation order.
+// key block, sub-tile, first slot, slot count.  Fixed summation order.  One
+// workgroup per (descriptor, batch x kv-head, 512-element chunk of the 64 x 128
+// tile); each thread sums two elements of dK and of dV over the slots.
+constexpr int RED_CHUNK = 512;
 template <int BW>
 __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     float* __restrict__ dK, float* __restrict__ dV, const float* __restrict__ part,
     const int32_t* __restrict__ reds, int32_t nslots, int32_t n, int32_t batch_hkv) {
+    constexpr int NCH = KT * BD / RED_CHUNK;
     const int32_t x = blockIdx.x;
-    const int32_t bh = x % batch_hkv;
-    const int32_t* rd = reds + 4 * (x / batch_hkv);
+    const int ch = x % NCH;
+    const int32_t bh = (x / NCH) % batch_hkv;
+    const int32_t* rd = reds + 4 * (x / NCH / batch_hkv);
     const int32_t i = rd[0], u = rd[1], s0 = rd[2], ns = rd[3];
     const int64_t kvrow0 = (int64_t)bh * n;
-    for (int e = threadIdx.x; e < KT * BD; e += blockDim.x) {
+#pragma unroll
+    for (int h = 0; h < RED_CHUNK / 256; ++h) {
+        const int e = ch * RED_CHUNK + h * 256 + threadIdx.x;
         const int key = e / BD, d = e % BD;
         const int32_t kp = i * BW + u * KT + key;
-        if (kp >= n) continue;
         float sk = 0.f, sv = 0.f;
         for (int32_t s = 0; s < ns; ++s) {
             const float* pk = part + (((int64_t)bh * nslots + s0 + s) * 2) * (KT * BD);
             sk += pk[e];
             sv += pk[KT * BD + e];
         }
-        dK[(kvrow0 + kp) * BD + d] = sk;
-        dV[(kvrow0 + kp) * BD + d] = sv;
+        if (kp < n) {
+            dK[(kvrow0 + kp) * BD + d] = sk;
+            dV[(kvrow0 + kp) * BD + d] = sv;
+        }
     }
 }
 
@@ -515,7 +523,9 @@ hipError_t launch_bwd_g(const BwdArgs& a, hipStream_t stream) {
         if (e != hipSuccess) return e;
     }
     if (a.nred > 0) {
-        hipLaunchKernelGGL((bwd_reduce_kernel<BW>), dim3((unsigned)(a.nred * bhk)), dim3(256), 0,
+        const int64_t grid = (int64_t)a.nred * bhk * (KT * BD / RED_CHUNK);
+        if (grid > 0x7fffffff) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((bwd_reduce_kernel<BW>), dim3((unsigned)grid), dim3(256), 0,
                            stream, a.dK, a.dV, a.part, a.reds, a.nslots, (int32_t)a.n, bhk);
         e = hipGetLastError();
     }
