@@ -19,6 +19,11 @@ The last line of stdout is one JSON record:
   dense      the in-house dense causal kernel timed with the paper's
              protocol (5 warmups, 30 reps, two opposite orders, median of the
              two order medians, §4.3) next to BF1 timed the same way
+  backward   the backward (dQ, dK, dV) of the same layer, timed with the
+             same two-order protocol next to the forward: one bf1_attn_bwd
+             call (Delta, dQ, dK/dV and the partial-sum reduce) per rep,
+             algorithmic TFLOP/s = 10 * head_dim * selected pairs * Hq * batch
+             / time, against the same bf16 MFMA peak
   cpu_baseline  the fp64 CPU oracle on a bounded sample of the workload
 
 --sweep additionally times n = 1K..64K for block widths 64 and 128 with the
@@ -54,6 +59,7 @@ def parse():
     ap.add_argument("--sweep-out", default=os.path.join(ROOT, "gpurun_out", "sweep.jsonl"))
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time bound of the CPU oracle sample")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
@@ -67,9 +73,13 @@ def parse():
 
 
 def kernel_source_hash():
+    """sha256 over the forward kernel's sources (the kernel file and the
+    device helpers it includes, in that order)."""
     import hashlib
-    path = os.path.join(ROOT, "paper_2608_20427_amd", "csrc", "bf1_kernels.hip")
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for name in ("bf1_kernels.hip", "bf1_device.h"):
+        h.update(open(os.path.join(ROOT, "paper_2608_20427_amd", "csrc", name), "rb").read())
+    return h.hexdigest()
 
 
 def timed_reps(torch, fn, warmup, reps):
@@ -163,6 +173,30 @@ def run_point(torch, bf1, w, q, k, v, warmup, reps, with_dense=True):
                     "speedup_vs_dense": sd["ms"] / sb["ms"],
                     "pair_reduction": dense_flops / flops})
     return rec
+
+
+def backward_point(torch, bf1, synth, w, q, k, v, warmup, reps):
+    """Two-order timing of the backward against the forward on one workload;
+    o and lse come from the forward, dO from the seeded generator."""
+    o, lse = bf1.attn_fwd(q, k, v, w.b, w.L)
+    do = synth.make_grad_out(w, device="cuda")
+    dq = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+    dk = torch.empty(k.shape, dtype=torch.float32, device="cuda")
+    dv = torch.empty(v.shape, dtype=torch.float32, device="cuda")
+    ws = torch.empty(bf1.bwd_workspace_size(w.batch, w.n, w.Hq, w.Hkv, w.d, w.b, w.L),
+                     dtype=torch.uint8, device="cuda")
+    f_bwd = lambda: bf1.attn_bwd(q, k, v, o, do, lse, w.b, w.L, dq=dq, dk=dk, dv=dv, workspace=ws)
+    f_fwd = lambda: bf1.attn_fwd(q, k, v, w.b, w.L, out=o, lse=lse)
+    sf, sb = two_order(torch, f_fwd, f_bwd, warmup, reps)
+    flops = bf1.selected_bwd_flops(w.batch, w.n, w.Hq, w.d, w.b, w.L)
+    tf = flops / sb["ms"] / 1e9
+    return {"workload": w.name, "bwd_ms": sb["ms"], "bwd_p10_ms": sb["p10"], "bwd_p90_ms": sb["p90"],
+            "fwd_ms": sf["ms"], "bwd_over_fwd": sb["ms"] / sf["ms"],
+            "bwd_algorithmic_gflop": flops / 1e9, "bwd_tflops": tf,
+            "bwd_pct_peak": 100 * tf / PEAK_BF16_TFLOPS,
+            "workspace_mb": ws.numel() / 1e6,
+            "kernels": "Delta+dQ (bwd_dq_kernel), dK/dV (bwd_dkdv_kernel), partial reduce "
+                       "(bwd_reduce_kernel); per-kernel times are in the rocprofv3 summary"}
 
 
 def main():
@@ -277,6 +311,12 @@ def main():
         rec["paper_protocol"] = point
         log(f"two-order protocol: bf1 {point['bf1_ms']:.4f} ms, dense {point.get('dense_ms', 0):.4f} ms,"
             f" speedup {point.get('speedup_vs_dense', 0):.2f}x")
+
+    if not args.no_backward:
+        bp = backward_point(torch, bf1, synth, w, q, k, v, args.warmup, args.reps)
+        rec["backward"] = bp
+        log(f"backward: {bp['bwd_ms']:.4f} ms ({bp['bwd_tflops']:.1f} TF/s, {bp['bwd_pct_peak']:.1f}%),"
+            f" forward {bp['fwd_ms']:.4f} ms, bwd/fwd {bp['bwd_over_fwd']:.2f}")
 
     if args.sweep:
         os.makedirs(os.path.dirname(args.sweep_out), exist_ok=True)
