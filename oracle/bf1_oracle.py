@@ -34,6 +34,15 @@ scale c = 1/sqrt(head_dim), these are the textbook softmax-attention
 gradients: dV = P^T dO, dP = dO V^T, dS = P * (dP - D), dQ = c dS K,
 dK = c dS^T Q, summed over the q-heads of a GQA group for dK and dV.
 
+Route variants (§4.3, §5.1, §5.2, Table 1): the paper's two topology
+controls at the same selected-pair budget as BF1 -- a contiguous local
+sliding window and a fixed ("static") random nonlocal graph -- plus the
+maximum shortest-path depth of any block route.  The paper names these
+controls but does not spell out their construction; the readings taken here
+are stated at route_sliding and route_static_random.  The random graph is
+parity-unpinned beyond its invariants (exact row sizes, locals kept,
+causality) and the published SplitMix64 outputs its draws come from.
+
 Attention: softmax with scale 1/sqrt(head_dim) and no score bias (§3.1,
 "no scale-dependent score bias"), restricted to the mask above.  q-head h
 reads kv-head h // (Hq / Hkv) (contiguous GQA groups).  Outputs are O
@@ -51,9 +60,16 @@ __all__ = [
     "route_table",
     "csr",
     "token_mask",
+    "token_mask_csr",
     "selected_pairs",
     "dense_pairs",
     "max_shortest_path",
+    "route_sliding",
+    "route_static_random",
+    "splitmix64",
+    "variant_csr",
+    "csr_pairs",
+    "max_shortest_path_csr",
     "attn_full_mask_fp64",
     "attn_gathered_fp64",
     "attn_csr_fp64",
@@ -136,6 +152,24 @@ def token_mask(n, b, L=2, rows=None):
     return allowed
 
 
+def token_mask_csr(n, b, row_ptr, col_idx):
+    """[n, n] boolean token mask of any causal block route in CSR form, by
+    the same rule as token_mask: earlier selected blocks fully visible, the
+    self block as a causal triangle with its diagonal."""
+    allowed = np.zeros((n, n), dtype=bool)
+    s = np.arange(n)
+    for t in range(n):
+        j = t // b
+        for i in col_idx[row_ptr[j]:row_ptr[j + 1]]:
+            i = int(i)
+            lo, hi = i * b, min((i + 1) * b, n)
+            if i < j:
+                allowed[t, lo:hi] = True
+            elif i == j:
+                allowed[t, lo:hi] = s[lo:hi] <= t
+    return allowed
+
+
 def selected_pairs(n, b, L=2):
     """Selected (query, key) token pairs per (batch, head), by enumeration.
 
@@ -164,9 +198,17 @@ def max_shortest_path(NB, L=2):
     block of the block graph whose edges are i -> j for i in P(j), i != j
     (the communication depth of §3.3, Proposition 2).  Breadth-first search
     from every source block."""
+    return _max_shortest_path_rows([route(j, L) for j in range(NB)])
+
+
+def _max_shortest_path_rows(rows):
+    """Breadth-first search from every source block over the edges i -> j
+    for i in rows[j], i != j; the largest distance to a later block.  Raises
+    if some later block cannot be reached at all."""
+    NB = len(rows)
     succ = [[] for _ in range(NB)]
     for j in range(NB):
-        for i in route(j, L):
+        for i in rows[j]:
             if i != j:
                 succ[i].append(j)
     worst = 0
@@ -185,6 +227,110 @@ def max_shortest_path(NB, L=2):
                 raise AssertionError(f"block {j} unreachable from {src}")
             worst = max(worst, dist[j])
     return worst
+
+
+# ---------------------------------------------------------------------------
+# Route variants at BF1's selected-pair budget (§4.3, §5.1, §5.2, Table 1)
+# ---------------------------------------------------------------------------
+
+_MASK64 = (1 << 64) - 1
+
+
+def splitmix64(seed, c):
+    """Output number c (c = 0, 1, ...) of the SplitMix64 generator seeded with
+    ``seed`` (Steele, Lea and Flood, "Fast splittable pseudorandom number
+    generators", OOPSLA 2014; the 64-bit finaliser constants of Vigna's
+    public-domain splitmix64).  The state after c + 1 steps is
+    seed + (c + 1) * 0x9E3779B97F4A7C15 mod 2^64, so any output can be
+    evaluated directly from its counter."""
+    z = (seed + (c + 1) * 0x9E3779B97F4A7C15) & _MASK64
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _MASK64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _MASK64
+    return z ^ (z >> 31)
+
+
+def route_sliding(j, L=2):
+    """Matched local sliding route of query block j: the |P(j)| most recent
+    blocks, j - |P(j)| + 1 .. j, ascending.
+
+    Reading: "equal-pair-count local sliding" (§4.3, §5.1; "contiguous
+    local", Table 1) keeps BF1's block count per query block, so every row
+    sees exactly as many key tokens as under Eq. 1 and the totals match.
+    This reading gives a maximum shortest path of 59 at 512 blocks, the
+    number §5.2 reports for matched sliding at 32K.
+    """
+    size = len(route(j, L))
+    return list(range(j - size + 1, j + 1))
+
+
+def route_static_random(j, L=2, seed=17):
+    """Matched static-random nonlocal route of query block j.
+
+    Reading (the paper fixes the seed, 17, and the budget but not the
+    construction, §4.4 and Table 1): the self block and its L local
+    predecessors are kept as in Eq. 1; BF1's nonlocal blocks (the global
+    block 0 and the dyadic ones, all earlier than j - L) are replaced by as
+    many distinct blocks drawn uniformly from 0 .. j - L - 1.  Row sizes, and
+    therefore the selected pairs, equal BF1's.
+
+    The draw is Floyd's sampling of k out of m = j - L candidates (Bentley
+    and Floyd, "A sample of brilliance", CACM 30(9), 1987): for t = 0..k-1
+    with r = m - k + t, take x uniform in [0, r]; add r if x was taken
+    before, else x.  Draw t of row j uses the SplitMix64 output with counter
+    j * 2^20 + t, mapped to [0, r] as (high 32 bits * (r + 1)) >> 32.
+    """
+    local = [i for i in range(j - L, j + 1) if i >= 0]
+    k = len(route(j, L)) - len(local)
+    m = j - L
+    taken = set()
+    for t in range(k):
+        r = m - k + t
+        x = ((splitmix64(seed, (j << 20) + t) >> 32) * (r + 1)) >> 32
+        taken.add(r if x in taken else x)
+    return sorted(taken | set(local))
+
+
+def variant_csr(kind, n, b, L=2, seed=17):
+    """CSR table (row_ptr[NB+1], col_idx) of a route: kind "bf1" (Eq. 1),
+    "sliding" or "static_random" (see route_sliding, route_static_random)."""
+    NB = num_blocks(n, b)
+    if kind == "bf1":
+        rows = [route(j, L) for j in range(NB)]
+    elif kind == "sliding":
+        rows = [route_sliding(j, L) for j in range(NB)]
+    elif kind == "static_random":
+        rows = [route_static_random(j, L, seed) for j in range(NB)]
+    else:
+        raise ValueError(f"unknown route kind {kind!r}")
+    row_ptr = np.zeros(NB + 1, dtype=np.int64)
+    for j, r in enumerate(rows):
+        row_ptr[j + 1] = row_ptr[j] + len(r)
+    col_idx = np.array([i for r in rows for i in r], dtype=np.int64)
+    return row_ptr.astype(np.int32), col_idx.astype(np.int32)
+
+
+def csr_pairs(n, b, row_ptr, col_idx):
+    """Selected (query, key) token pairs per (batch, head) of any causal
+    block route in CSR form, counted block pair by block pair as in
+    selected_pairs."""
+    total = 0
+    for j in range(len(row_ptr) - 1):
+        rows_j = min((j + 1) * b, n) - j * b
+        for i in col_idx[row_ptr[j]:row_ptr[j + 1]]:
+            i = int(i)
+            if i < j:
+                total += rows_j * (min((i + 1) * b, n) - i * b)
+            elif i == j:
+                total += rows_j * (rows_j + 1) // 2
+    return total
+
+
+def max_shortest_path_csr(row_ptr, col_idx):
+    """Communication depth (§3.3, §5.2) of any block route in CSR form: the
+    largest shortest-path length from a block to a later block."""
+    NB = len(row_ptr) - 1
+    return _max_shortest_path_rows(
+        [[int(i) for i in col_idx[row_ptr[j]:row_ptr[j + 1]]] for j in range(NB)])
 
 
 # ---------------------------------------------------------------------------
@@ -212,12 +358,13 @@ def _softmax_rows(x, vals):
     return w @ vals, lse[..., 0]
 
 
-def attn_full_mask_fp64(q, k, v, b, L=2, scale=None):
+def attn_full_mask_fp64(q, k, v, b, L=2, scale=None, mask=None):
     """Form (i): materialise the n x n token mask and run a masked softmax.
 
     For small n only (memory is n^2 per head).  Inputs are float arrays in
     [batch, H, n, d] layout; returns (O float64 [batch, Hq, n, d],
-    LSE float64 [batch, Hq, n], natural log).
+    LSE float64 [batch, Hq, n], natural log).  ``mask`` replaces the BF1
+    mask by another [n, n] boolean token mask (e.g. token_mask_csr).
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -226,7 +373,8 @@ def attn_full_mask_fp64(q, k, v, b, L=2, scale=None):
     if scale is None:
         scale = 1.0 / math.sqrt(d)
     G = Hq // Hkv
-    mask = token_mask(n, b, L)
+    if mask is None:
+        mask = token_mask(n, b, L)
     out = np.zeros((batch, Hq, n, d))
     lse = np.zeros((batch, Hq, n))
     for beta in range(batch):

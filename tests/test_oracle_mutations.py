@@ -8,6 +8,7 @@ import pytest
 
 import test_oracle_attention as TA
 import test_oracle_route as TR
+import test_oracle_variants as TV
 from oracle import bf1_oracle as orc
 
 _route = orc.route
@@ -171,3 +172,79 @@ BWD_PINS = [
 def test_backward_mutations_are_caught(monkeypatch, bad):
     monkeypatch.setattr(orc, "_bwd_gathered", bad)
     assert run_pins(BWD_PINS)
+
+
+# ---------------------------------------------------------------------------
+# Route variants and the depth search
+# ---------------------------------------------------------------------------
+
+_splitmix = orc.splitmix64
+
+
+def sliding_one_too_wide(j, L=2):
+    size = len(_route(j, L)) + 1
+    return list(range(max(0, j - size + 1), j + 1))
+
+
+def sliding_skips_self(j, L=2):
+    size = len(_route(j, L))
+    return list(range(j - size, j)) if j >= size else list(range(j + 1))
+
+
+def random_half_open_draw(j, L=2, seed=17):
+    local = [i for i in range(j - L, j + 1) if i >= 0]
+    k = len(_route(j, L)) - len(local)
+    taken = set()
+    for t in range(k):
+        r = j - L - k + t
+        x = ((_splitmix(seed, (j << 20) + t) >> 32) * r) >> 32     # [0, r) instead of [0, r]
+        taken.add(r if x in taken else x)
+    return sorted(taken | set(local))
+
+
+def random_drops_locals(j, L=2, seed=17):
+    row = _random(j, L, seed)
+    return sorted(set(row) - {j - 1})
+
+
+def splitmix_wrong_shift(seed, c):
+    z = (seed + (c + 1) * 0x9E3779B97F4A7C15) & ((1 << 64) - 1)
+    z = ((z ^ (z >> 31)) * 0xBF58476D1CE4E5B9) & ((1 << 64) - 1)
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & ((1 << 64) - 1)
+    return z ^ (z >> 31)
+
+
+_random = orc.route_static_random
+
+VARIANT_PINS = [
+    (TV.test_splitmix64_published_outputs, ()),
+    (TV.test_sliding_hand_rows, ()),
+    (TV.test_depth_golden, ("sliding", "512", "2", "59")),
+    (TV.test_variant_pairs_equal_bf1_and_mask, ("sliding", 777, 16, 2)),
+    (TV.test_variant_pairs_equal_bf1_and_mask, ("static_random", 777, 16, 2)),
+    (TV.test_variant_rows_valid, (2,)),
+    (TV.test_static_random_is_uniform_over_candidates, ()),
+]
+
+
+@pytest.mark.parametrize("name,bad", [("route_sliding", sliding_one_too_wide),
+                                      ("route_sliding", sliding_skips_self),
+                                      ("route_static_random", random_half_open_draw),
+                                      ("route_static_random", random_drops_locals),
+                                      ("splitmix64", splitmix_wrong_shift)])
+def test_variant_mutations_are_caught(monkeypatch, name, bad):
+    monkeypatch.setattr(orc, name, bad)
+    assert run_pins(VARIANT_PINS)
+
+
+def bfs_off_by_one(rows):
+    return _depth_rows(rows) + 1
+
+
+_depth_rows = orc._max_shortest_path_rows
+
+
+def test_depth_mutation_is_caught(monkeypatch):
+    monkeypatch.setattr(orc, "_max_shortest_path_rows", bfs_off_by_one)
+    assert run_pins([(TV.test_depth_bfs_matches_minplus, ("sliding", 40, 2)),
+                     (TV.test_depth_golden, ("bf1", "512", "2", "8"))])
