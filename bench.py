@@ -24,6 +24,11 @@ The last line of stdout is one JSON record:
              call (Delta, dQ, dK/dV and the partial-sum reduce) per rep,
              algorithmic TFLOP/s = 10 * head_dim * selected pairs * Hq * batch
              / time, against the same bf16 MFMA peak
+  route_variants  the same kernel (bf1_attn_fwd_csr) over BF1's table and
+             the two equal-pair-count controls of §4.3 / §5.1 (matched local
+             sliding, static random graph seed 17), timed with the paper
+             protocol extended to three routes (orders A,B,C then C,B,A),
+             each with its communication depth (§5.2)
   cpu_baseline  the fp64 CPU oracle on a bounded sample of the workload
 
 --sweep additionally times n = 1K..64K for block widths 64 and 128 with the
@@ -60,6 +65,7 @@ def parse():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true")
+    ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time bound of the CPU oracle sample")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
@@ -199,6 +205,34 @@ def backward_point(torch, bf1, synth, w, q, k, v, warmup, reps):
                        "(bwd_reduce_kernel); per-kernel times are in the rocprofv3 summary"}
 
 
+def variants_point(torch, bf1, w, q, k, v, warmup, reps):
+    """BF1, matched sliding and static-random tables through the CSR kernel:
+    every table has BF1's pair count, so equal times mean cost tracks pairs
+    and not topology (§5.1)."""
+    o = torch.empty_like(q)
+    lse = torch.empty((w.batch, w.Hq, w.n), dtype=torch.float32, device="cuda")
+    kinds = ["bf1", "sliding", "static_random"]
+    tables, depth = {}, {}
+    for kd in kinds:
+        rp, ci = bf1.plan_variant(kd, w.n, w.b, w.L, 17)
+        depth[kd] = bf1.route_depth(rp, ci) if len(rp) - 1 <= 16384 else None
+        tables[kd] = (torch.from_numpy(rp).cuda(), torch.from_numpy(ci).cuda())
+    fns = {kd: (lambda t=tables[kd]: bf1.attn_fwd_csr(q, k, v, w.b, t[0], t[1], out=o, lse=lse))
+           for kd in kinds}
+    runs = {kd: [] for kd in kinds}
+    for order in (kinds, kinds[::-1]):
+        for kd in order:
+            runs[kd].append(timed_reps(torch, fns[kd], warmup, reps))
+    flops = bf1.selected_flops(w.batch, w.n, w.Hq, w.d, w.b, w.L)
+    out = {"workload": w.name, "seed": 17, "selected_gflop": flops / 1e9}
+    for kd in kinds:
+        ms = statistics.median([statistics.median(x) for x in runs[kd]])
+        out[kd] = {"ms": ms, "tflops": flops / ms / 1e9, "max_shortest_path": depth[kd]}
+    for kd in kinds[1:]:
+        out[kd]["time_vs_bf1"] = out[kd]["ms"] / out["bf1"]["ms"]
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -317,6 +351,13 @@ def main():
         rec["backward"] = bp
         log(f"backward: {bp['bwd_ms']:.4f} ms ({bp['bwd_tflops']:.1f} TF/s, {bp['bwd_pct_peak']:.1f}%),"
             f" forward {bp['fwd_ms']:.4f} ms, bwd/fwd {bp['bwd_over_fwd']:.2f}")
+
+    if not args.no_variants:
+        vp = variants_point(torch, bf1, w, q, k, v, args.warmup, args.reps)
+        rec["route_variants"] = vp
+        log("route variants: " + ", ".join(
+            f"{kd} {vp[kd]['ms']:.4f} ms (depth {vp[kd]['max_shortest_path']})"
+            for kd in ("bf1", "sliding", "static_random")))
 
     if args.sweep:
         os.makedirs(os.path.dirname(args.sweep_out), exist_ok=True)

@@ -164,6 +164,49 @@ int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, con
                  int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
                  int32_t B, int32_t L, void* workspace, int64_t workspace_bytes, void* stream);
 
+/*
+ * Route variants at BF1's selected-pair budget (host only, no device work):
+ * the topology controls the paper times against BF1 (§4.3, §5.1) and
+ * compares by communication depth (§5.2, Table 1).  Every variant keeps
+ * |P(j)| blocks in row j (self block included, rows ascending), so its CSR
+ * size and its selected pairs equal BF1's (bf1_plan_size) and its tables run
+ * unchanged through bf1_attn_fwd_csr.
+ *   BF1_ROUTE_BF1           Eq. 1 itself (the table bf1_plan writes).
+ *   BF1_ROUTE_SLIDING       matched local sliding: blocks j-|P(j)|+1 .. j.
+ *   BF1_ROUTE_STATIC_RANDOM static random nonlocal graph: the self block and
+ *       the L local predecessors of Eq. 1 stay; BF1's other blocks (global
+ *       and dyadic, all before j-L) are replaced by as many distinct blocks
+ *       drawn uniformly from 0 .. j-L-1 with Floyd's sampling; draw t of row j
+ *       is SplitMix64 output number j*2^20 + t of the generator seeded with
+ *       `seed` (the paper's graph uses seed 17), mapped to [0, r] as
+ *       (high 32 bits * (r+1)) >> 32.  `seed` is ignored by the other kinds.
+ *   row_ptr : HOST int32[NB + 1]; col_idx : HOST int32[col_capacity].
+ * Returns BF1_ERR_INVALID_ARG for an unknown kind or bad sizes,
+ * BF1_ERR_BUFFER_TOO_SMALL if col_capacity < nnz.
+ */
+typedef enum {
+    BF1_ROUTE_BF1 = 0,
+    BF1_ROUTE_SLIDING = 1,
+    BF1_ROUTE_STATIC_RANDOM = 2
+} bf1_route_kind;
+
+int bf1_plan_variant(int32_t kind, int64_t n, int32_t B, int32_t L, uint64_t seed,
+                     int32_t* row_ptr, int32_t* col_idx, int64_t col_capacity);
+
+/*
+ * Communication depth of a causal block route (host only; §3.3 Prop. 2 and
+ * §5.2): the largest, over pairs of blocks i < j, of the fewest hops from i
+ * to j along edges i -> j' for every earlier block i in row j' of the table.
+ *   row_ptr : HOST int32[num_blocks + 1], row_ptr[0] = 0, non-decreasing;
+ *   col_idx : HOST int32[row_ptr[num_blocks]], every entry of row j in [0, j].
+ *   max_depth <- the depth, or -1 if some later block is unreachable.
+ * Breadth-first search from every block: O(num_blocks * (num_blocks + nnz))
+ * time, num_blocks <= 16384.  Returns BF1_ERR_INVALID_ARG on a malformed or
+ * non-causal table.
+ */
+int bf1_route_depth(const int32_t* row_ptr, const int32_t* col_idx, int32_t num_blocks,
+                    int32_t* max_depth);
+
 /* Frees every cached plan (device memory owned by the library).  Must not
  * race with in-flight bf1_attn_fwd / bf1_attn_bwd calls that use those plans. */
 void bf1_release_plans(void);

@@ -79,6 +79,10 @@ def load():
     lib.bf1_attn_bwd.restype = ctypes.c_int
     lib.bf1_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i32, i64, i32, i32, i32,
                                  i32, i32, vp, i64, vp]
+    lib.bf1_plan_variant.restype = ctypes.c_int
+    lib.bf1_plan_variant.argtypes = [i32, i64, i32, i32, ctypes.c_uint64, vp, vp, i64]
+    lib.bf1_route_depth.restype = ctypes.c_int
+    lib.bf1_route_depth.argtypes = [vp, vp, i32, ctypes.POINTER(i32)]
     _LIB = lib
     return lib
 
@@ -207,6 +211,40 @@ def plan_transposed(n, B=64, L=2):
                                       col_idx.ctypes.data_as(ctypes.c_void_p), col_idx.size),
            "bf1_plan_transposed")
     return row_ptr, col_idx[:nnz]
+
+
+ROUTE_KINDS = {"bf1": 0, "sliding": 1, "static_random": 2}
+
+
+def plan_variant(kind, n, B=64, L=2, seed=17):
+    """Route table (host numpy int32 row_ptr[NB+1], col_idx) of kind "bf1",
+    "sliding" (matched local sliding) or "static_random" (static random
+    nonlocal graph drawn from `seed`); every kind has BF1's row sizes."""
+    import numpy as np
+    if kind not in ROUTE_KINDS:
+        raise ValueError(f"unknown route kind {kind!r}; one of {sorted(ROUTE_KINDS)}")
+    nb, nnz, _ = plan_size(n, B, L)
+    row_ptr = np.zeros(nb + 1, dtype=np.int32)
+    col_idx = np.zeros(max(nnz, 1), dtype=np.int32)
+    _check(load().bf1_plan_variant(ROUTE_KINDS[kind], int(n), int(B), int(L), int(seed),
+                                   row_ptr.ctypes.data_as(ctypes.c_void_p),
+                                   col_idx.ctypes.data_as(ctypes.c_void_p), col_idx.size),
+           "bf1_plan_variant")
+    return row_ptr, col_idx[:nnz]
+
+
+def route_depth(row_ptr, col_idx):
+    """Communication depth (largest shortest path between blocks) of a host
+    CSR route table; -1 if some later block is unreachable."""
+    import numpy as np
+    rp = np.ascontiguousarray(row_ptr, dtype=np.int32)
+    ci = np.ascontiguousarray(col_idx, dtype=np.int32)
+    if ci.size == 0:
+        ci = np.zeros(1, dtype=np.int32)
+    out = ctypes.c_int32(0)
+    _check(load().bf1_route_depth(rp.ctypes.data_as(ctypes.c_void_p), ci.ctypes.data_as(ctypes.c_void_p),
+                                  int(rp.size - 1), ctypes.byref(out)), "bf1_route_depth")
+    return out.value
 
 
 def bwd_workspace_size(batch, n, Hq, Hkv, d=128, B=64, L=2):

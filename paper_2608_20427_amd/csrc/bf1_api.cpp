@@ -312,6 +312,90 @@ int bf1_plan_transposed(int64_t n, int32_t B, int32_t L, int32_t* row_ptr, int32
     return e == nnz ? BF1_OK : BF1_ERR_INVALID_ARG;
 }
 
+int bf1_plan_variant(int32_t kind, int64_t n, int32_t B, int32_t L, uint64_t seed, int32_t* row_ptr,
+                     int32_t* col_idx, int64_t col_capacity) {
+    if (kind != BF1_ROUTE_BF1 && kind != BF1_ROUTE_SLIDING && kind != BF1_ROUTE_STATIC_RANDOM)
+        return BF1_ERR_INVALID_ARG;
+    if (n < 0 || B < 1 || L < 0 || col_capacity < 0 || !row_ptr) return BF1_ERR_INVALID_ARG;
+    int64_t NB, nnz;
+    if (!route_sizes(n, B, L, &NB, &nnz)) return BF1_ERR_INVALID_ARG;
+    if (nnz > 0 && !col_idx) return BF1_ERR_INVALID_ARG;
+    if (col_capacity < nnz) return BF1_ERR_BUFFER_TOO_SMALL;
+    int64_t e = 0;
+    for (int64_t j = 0; j < NB; ++j) {
+        row_ptr[j] = (int32_t)e;
+        if (kind == BF1_ROUTE_BF1) {
+            // Eq. 1, ascending: block 0, dyadics from the farthest, locals, self
+            const int64_t start = e;
+            if (j > L) col_idx[e++] = 0;
+            int r = 2;
+            while (r < 62 && (int64_t(1) << (r + 1)) <= j) ++r;
+            for (; r >= 2; --r) {
+                const int64_t off = int64_t(1) << r;
+                if (off <= j && off > L && j - off > 0) col_idx[e++] = (int32_t)(j - off);
+            }
+            for (int64_t t = (j - L > 0 ? j - L : 0); t <= j; ++t) col_idx[e++] = (int32_t)t;
+            if (e - start != 1 + bf1::route_pred_count(j, L)) return BF1_ERR_INVALID_ARG;
+        } else if (kind == BF1_ROUTE_SLIDING) {
+            e += bf1::route_sliding_row(j, L, col_idx + e);
+        } else {
+            e += bf1::route_static_random_row(j, L, seed, col_idx + e);
+        }
+    }
+    row_ptr[NB] = (int32_t)e;
+    return e == nnz ? BF1_OK : BF1_ERR_INVALID_ARG;
+}
+
+int bf1_route_depth(const int32_t* row_ptr, const int32_t* col_idx, int32_t num_blocks,
+                    int32_t* max_depth) {
+    if (num_blocks < 0 || num_blocks > 16384 || !row_ptr || !max_depth) return BF1_ERR_INVALID_ARG;
+    const int32_t NB = num_blocks;
+    if (row_ptr[0] != 0) return BF1_ERR_INVALID_ARG;
+    for (int32_t j = 0; j < NB; ++j)
+        if (row_ptr[j + 1] < row_ptr[j]) return BF1_ERR_INVALID_ARG;
+    if (row_ptr[NB] > 0 && !col_idx) return BF1_ERR_INVALID_ARG;
+    // successor lists: edge i -> j for every earlier block i in row j
+    std::vector<int32_t> deg(NB + 1, 0);
+    for (int32_t j = 0; j < NB; ++j)
+        for (int32_t e = row_ptr[j]; e < row_ptr[j + 1]; ++e) {
+            const int32_t i = col_idx[e];
+            if (i < 0 || i > j) return BF1_ERR_INVALID_ARG;
+            if (i < j) ++deg[i + 1];
+        }
+    for (int32_t i = 0; i < NB; ++i) deg[i + 1] += deg[i];
+    std::vector<int32_t> succ(deg[NB]), fill(deg.begin(), deg.end() - 1);
+    for (int32_t j = 0; j < NB; ++j)
+        for (int32_t e = row_ptr[j]; e < row_ptr[j + 1]; ++e)
+            if (col_idx[e] < j) succ[fill[col_idx[e]]++] = j;
+    // breadth-first search from every source; edges only go forward, so a
+    // source's search touches blocks src..NB-1 only
+    std::vector<int32_t> dist(NB), queue(NB);
+    int32_t worst = 0;
+    for (int32_t src = 0; src < NB; ++src) {
+        std::fill(dist.begin() + src, dist.end(), -1);
+        dist[src] = 0;
+        int32_t head = 0, tail = 0;
+        queue[tail++] = src;
+        while (head < tail) {
+            const int32_t u = queue[head++];
+            for (int32_t e = deg[u]; e < deg[u + 1]; ++e) {
+                const int32_t w = succ[e];
+                if (dist[w] < 0) {
+                    dist[w] = dist[u] + 1;
+                    queue[tail++] = w;
+                }
+            }
+        }
+        if (tail != NB - src) {
+            *max_depth = -1;
+            return BF1_OK;
+        }
+        worst = std::max(worst, dist[queue[tail - 1]]);
+    }
+    *max_depth = worst;
+    return BF1_OK;
+}
+
 int bf1_attn_bwd_workspace_size(int32_t batch, int64_t n, int32_t Hq, int32_t Hkv,
                                 int32_t head_dim, int32_t B, int32_t L, int64_t* bytes) {
     if (!bytes) return BF1_ERR_INVALID_ARG;

@@ -101,4 +101,56 @@ inline int64_t route_users(int64_t NB, int64_t L, int64_t i, int32_t* out) {
     return c;
 }
 
+// ---- Route variants at BF1's selected-pair budget (§4.3, §5.1, Table 1) ----
+// Both keep |P(j)| blocks in every row, so every query token sees exactly as
+// many keys as under Eq. 1 and the totals (pairs, CSR size) are BF1's.
+
+// Output number c (from 0) of SplitMix64 seeded with `seed` (Steele, Lea and
+// Flood, OOPSLA 2014): the state after c + 1 steps of adding the golden-ratio
+// increment, put through the generator's 64-bit finaliser.
+inline uint64_t splitmix64_at(uint64_t seed, uint64_t c) {
+    uint64_t z = seed + (c + 1) * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// Contiguous local sliding route: the |P(j)| most recent blocks up to j.
+inline int64_t route_sliding_row(int64_t j, int64_t L, int32_t* out) {
+    const int64_t size = 1 + route_pred_count(j, L);
+    for (int64_t t = 0; t < size; ++t) out[t] = (int32_t)(j - size + 1 + t);
+    return size;
+}
+
+// Static random nonlocal route: the self block and its L local predecessors
+// stay; the remaining k = |P(j)| - (locals + 1) entries are distinct blocks
+// drawn uniformly from 0 .. j-L-1 by Floyd's k-of-m sampling (Bentley and
+// Floyd, CACM 1987): for t < k, with r = m - k + t, draw x in [0, r] and
+// keep r if x is already chosen, else x.  Draw t of row j uses SplitMix64
+// output j * 2^20 + t, mapped to [0, r] by (high 32 bits * (r + 1)) >> 32.
+// Row written ascending; returns its length.
+inline int64_t route_static_random_row(int64_t j, int64_t L, uint64_t seed, int32_t* out) {
+    const int64_t lo = j - L > 0 ? j - L : 0;
+    const int64_t size = 1 + route_pred_count(j, L);
+    const int64_t k = size - (j - lo + 1);
+    const int64_t m = j - L;
+    int64_t c = 0;
+    for (int64_t t = 0; t < k; ++t) {
+        const uint64_t r = (uint64_t)(m - k + t);
+        const uint64_t x = ((splitmix64_at(seed, ((uint64_t)j << 20) + (uint64_t)t) >> 32) * (r + 1)) >> 32;
+        bool seen = false;
+        for (int64_t a = 0; a < c; ++a) seen |= (uint64_t)out[a] == x;
+        out[c++] = (int32_t)(seen ? r : x);
+    }
+    // insertion sort of the k drawn blocks (k < 64)
+    for (int64_t a = 1; a < c; ++a) {
+        const int32_t v = out[a];
+        int64_t b = a;
+        for (; b > 0 && out[b - 1] > v; --b) out[b] = out[b - 1];
+        out[b] = v;
+    }
+    for (int64_t i = lo; i <= j; ++i) out[c++] = (int32_t)i;
+    return c;
+}
+
 }  // namespace bf1

@@ -10,6 +10,7 @@ import re
 import pytest
 
 import paper_2608_20427_amd as bf1
+from conftest import read_golden
 from oracle import bf1_oracle as orc
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -160,3 +161,73 @@ def test_backward_invalid_arguments_rejected_without_device(lib):
     assert lib.bf1_plan_transposed(4096, 64, 2, rp.ctypes.data_as(ctypes.c_void_p),
                                    ci.ctypes.data_as(ctypes.c_void_p), nnz - 1) == \
         bf1.BF1_ERR_BUFFER_TOO_SMALL
+
+
+# ---- route variants and the depth tool (host entry points) -------------------
+
+VARIANT_CASES = [(1, 64, 2), (257, 64, 2), (4096, 64, 2), (32768, 64, 2), (30001, 64, 2),
+                 (65536, 128, 2), (512, 64, 1), (5000, 7, 0), (777, 16, 3), (3000, 8, 5)]
+
+
+def test_header_declares_the_variants():
+    names = declared_functions()
+    for want in ["bf1_plan_variant", "bf1_route_depth"]:
+        assert want in names
+
+
+@pytest.mark.parametrize("kind", ["bf1", "sliding", "static_random"])
+@pytest.mark.parametrize("n,B,L", VARIANT_CASES)
+def test_plan_variant_matches_oracle(lib, kind, n, B, L):
+    for seed in (17, 2 ** 64 - 1, 0):
+        rp, ci = bf1.plan_variant(kind, n, B, L, seed)
+        rp_o, ci_o = orc.variant_csr(kind, n, B, L, seed)
+        assert rp.tolist() == rp_o.tolist(), seed
+        assert ci.tolist() == ci_o.tolist(), seed
+        if kind != "static_random":
+            break
+
+
+@pytest.mark.parametrize("n,B,L", VARIANT_CASES[:6])
+def test_plan_variant_bf1_equals_planner_table(lib, n, B, L):
+    rp, ci = bf1.plan_variant("bf1", n, B, L)
+    rp_o, ci_o = orc.csr(n, B, L)
+    assert rp.tolist() == rp_o.tolist() and ci.tolist() == ci_o.tolist()
+
+
+@pytest.mark.parametrize("kind", ["bf1", "sliding", "static_random"])
+@pytest.mark.parametrize("NB,B,L", [(1, 64, 2), (2, 64, 2), (40, 16, 2), (300, 4, 1), (512, 64, 2),
+                                    (1024, 64, 2), (200, 8, 4)])
+def test_route_depth_matches_oracle(lib, kind, NB, B, L):
+    rp, ci = bf1.plan_variant(kind, NB * B, B, L, 17)
+    assert bf1.route_depth(rp, ci) == orc.max_shortest_path_csr(*orc.variant_csr(kind, NB * B, B, L, 17))
+
+
+def test_route_depth_golden(lib):
+    for route_kind, NB, L, depth in read_golden("route_variant_depth.txt"):
+        rp, ci = bf1.plan_variant(route_kind, int(NB) * 64, 64, int(L))
+        assert bf1.route_depth(rp, ci) == int(depth)
+
+
+def test_route_depth_unreachable_and_invalid(lib):
+    import numpy as np
+    # rows {0}, {1}, {1, 2}: block 2 is unreachable from block 0
+    rp = np.array([0, 1, 2, 4], dtype=np.int32)
+    ci = np.array([0, 1, 1, 2], dtype=np.int32)
+    assert bf1.route_depth(rp, ci) == -1
+    out = ctypes.c_int32(7)
+    vp = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    # a future block in row 1, a decreasing row_ptr, too many blocks
+    bad = np.array([0, 2, 3], dtype=np.int32)
+    assert lib.bf1_route_depth(vp(np.array([0, 1, 3], dtype=np.int32)), vp(bad), 2, ctypes.byref(out)) == \
+        bf1.BF1_ERR_INVALID_ARG
+    assert lib.bf1_route_depth(vp(np.array([0, 2, 1], dtype=np.int32)), vp(ci), 2, ctypes.byref(out)) == \
+        bf1.BF1_ERR_INVALID_ARG
+    assert lib.bf1_route_depth(vp(rp), vp(ci), 16385, ctypes.byref(out)) == bf1.BF1_ERR_INVALID_ARG
+    assert out.value == 7
+    # unknown kind, capacity
+    r = np.zeros(70, dtype=np.int32)
+    c = np.zeros(500, dtype=np.int32)
+    assert lib.bf1_plan_variant(3, 4096, 64, 2, 17, vp(r), vp(c), 500) == bf1.BF1_ERR_INVALID_ARG
+    assert lib.bf1_plan_variant(1, 4096, 64, 2, 17, vp(r), vp(c), 441) == bf1.BF1_ERR_BUFFER_TOO_SMALL
+    with pytest.raises(ValueError):
+        bf1.plan_variant("dilated", 4096)
