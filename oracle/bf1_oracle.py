@@ -43,6 +43,14 @@ are stated at route_sliding and route_static_random.  The random graph is
 parity-unpinned beyond its invariants (exact row sizes, locals kept,
 causality) and the published SplitMix64 outputs its draws come from.
 
+Decode (§3.2, last paragraph; §4.2 "cached one-token decode"; §5.4): the
+token at position t = seq_len - 1 of a sequence attends to the same keys as
+row t of the prefill mask -- the earlier selected blocks of its block
+j = t // b in full, and its own block up to t -- read from a cache of
+earlier keys and values.  decode_plan lists the physical pages (blocks)
+such a token reads through a page table; attn_decode_fp64 is the attention
+row itself.
+
 Attention: softmax with scale 1/sqrt(head_dim) and no score bias (§3.1,
 "no scale-dependent score bias"), restricted to the mask above.  q-head h
 reads kv-head h // (Hq / Hkv) (contiguous GQA groups).  Outputs are O
@@ -75,6 +83,8 @@ __all__ = [
     "attn_csr_fp64",
     "dense_causal_fp64",
     "csr_transposed",
+    "decode_plan",
+    "attn_decode_fp64",
     "attn_bwd_csr_fp64",
     "attn_bwd_gathered_fp64",
     "attn_bwd_abs_terms_fp64",
@@ -609,3 +619,51 @@ def attn_bwd_abs_terms_fp64(q, k, v, do, b, L=2, scale=None, q_blocks=None, kv_b
     core = {"ds": _bwd_abs_terms, "pdp": _bwd_abs_terms_pdp}[kind]
     return attn_bwd_csr_fp64(q, k, v, do, b, row_ptr, col_idx, scale=scale, q_blocks=q_blocks,
                              kv_blocks=kv_blocks, o=o, _core=core)
+
+
+# ---------------------------------------------------------------------------
+# One-token decode (§3.2, §4.2, §5.4)
+# ---------------------------------------------------------------------------
+
+def decode_plan(seq_len, page_row, b, L=2, dense=False):
+    """Pages read by the newest token of a sequence of seq_len tokens whose
+    logical block i lives in physical page page_row[i]: returns (j, earlier)
+    with j = (seq_len - 1) // b the token's block and ``earlier`` the physical
+    pages of the selected blocks before j (P(j) without j, ascending by
+    logical block; every earlier block for ``dense``).  The self page is
+    page_row[j]."""
+    if seq_len < 1:
+        raise ValueError("a decode step needs at least one token")
+    j = (seq_len - 1) // b
+    blocks = range(j) if dense else [i for i in route(j, L) if i < j]
+    return j, [int(page_row[i]) for i in blocks]
+
+
+def attn_decode_fp64(q, k, v, seq_lens, b, L=2, scale=None):
+    """Attention of each sequence's newest token (position t = seq_len - 1).
+
+    q: [batch, Hq, d] (the newest token's query per q-head); k, v:
+    [batch, Hkv, n_max, d] logical key/value caches (positions >= seq_len are
+    ignored).  Row t of the §3.1 token mask over seq_len tokens decides which
+    keys are visible; returns (O [batch, Hq, d], LSE [batch, Hq]) in float64.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    batch, Hq, d = q.shape
+    Hkv = k.shape[1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    G = Hq // Hkv
+    out = np.zeros((batch, Hq, d))
+    lse = np.zeros((batch, Hq))
+    for beta in range(batch):
+        n = int(seq_lens[beta])
+        t = n - 1
+        keys = np.nonzero(token_mask(n, b, L, rows=[t])[0])[0]
+        for h in range(Hq):
+            g = h // G
+            x = scale * (k[beta, g, keys] @ q[beta, h])
+            o, l = _softmax_rows(x[None, :], v[beta, g, keys])
+            out[beta, h], lse[beta, h] = o[0], l[0]
+    return out, lse

@@ -248,3 +248,42 @@ def test_depth_mutation_is_caught(monkeypatch):
     monkeypatch.setattr(orc, "_max_shortest_path_rows", bfs_off_by_one)
     assert run_pins([(TV.test_depth_bfs_matches_minplus, ("sliding", 40, 2)),
                      (TV.test_depth_golden, ("bf1", "512", "2", "8"))])
+
+
+# ---------------------------------------------------------------------------
+# Decode
+# ---------------------------------------------------------------------------
+
+import test_oracle_decode as TD
+
+_decode = orc.attn_decode_fp64
+_decode_plan = orc.decode_plan
+
+
+def decode_previous_row(q, k, v, seq_lens, b, L=2, scale=None):
+    # reads the keys of row t - 1 (a stale mask row) for sequences longer than one token
+    return _decode(q, k, v, [max(1, int(n) - 1) for n in seq_lens], b, L, scale)
+
+
+def decode_plan_with_self(seq_len, page_row, b, L=2, dense=False):
+    j, earlier = _decode_plan(seq_len, page_row, b, L, dense)
+    return j, earlier + [int(page_row[j])]
+
+
+def decode_plan_next_block(seq_len, page_row, b, L=2, dense=False):
+    return _decode_plan(seq_len + b, page_row, b, L, dense)
+
+
+DECODE_PINS = [
+    (TD.test_decode_equals_last_row_of_full_mask_forward, (16, 2)),
+    (TD.test_decode_zero_keys_closed_form, (1000,)),
+    (TD.test_decode_plan_counts_and_mapping, (2,)),
+]
+
+
+@pytest.mark.parametrize("name,bad", [("attn_decode_fp64", decode_previous_row),
+                                      ("decode_plan", decode_plan_with_self),
+                                      ("decode_plan", decode_plan_next_block)])
+def test_decode_mutations_are_caught(monkeypatch, name, bad):
+    monkeypatch.setattr(orc, name, bad)
+    assert run_pins(DECODE_PINS)
