@@ -29,6 +29,13 @@ The last line of stdout is one JSON record:
              sliding, static random graph seed 17), timed with the paper
              protocol extended to three routes (orders A,B,C then C,B,A),
              each with its communication depth (§5.2)
+  decode     one-token decode over a paged cache (§5.4, Table 3): contexts
+             32K / 64K, batch 1 / 8 / 32, a plan per route epoch; the step
+             (split + merge kernels) and the planner timed as replayed HIP
+             graphs (device time, as a serving loop runs them) and eagerly
+             (host launch included); the dense decode through the same
+             kernels next to it; achieved HBM GB/s on the algorithmic bytes
+             (the K/V rows each token reads, its query and output)
   cpu_baseline  the fp64 CPU oracle on a bounded sample of the workload
 
 --sweep additionally times n = 1K..64K for block widths 64 and 128 with the
@@ -66,6 +73,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--no-variants", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time bound of the CPU oracle sample")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
@@ -233,6 +241,66 @@ def variants_point(torch, bf1, w, q, k, v, warmup, reps):
     return out
 
 
+def graph_ms(torch, fn, replays, inner=32):
+    """Device time per call of fn: `inner` calls captured in one HIP graph,
+    the graph replayed back to back; host launch cost is paid once per
+    replay and spread over the inner calls."""
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(inner):
+            fn()
+    for _ in range(2):
+        g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(replays):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / (replays * inner)
+
+
+def decode_point(torch, bf1, synth, w, reps):
+    """BF1 and dense decode steps over the same paged cache."""
+    q, kp, vp, sl, table, num_pages = synth.make_decode_device(w)
+    o = torch.empty_like(q)
+    lse = torch.empty((w.batch, w.Hq), dtype=torch.float32, device="cuda")
+    rec = {"workload": w.name, "batch": w.batch, "context": w.ctx, "Hq": w.Hq, "Hkv": w.Hkv,
+           "head_dim": w.d, "block_width": w.b, "local_blocks": w.L}
+    for dense in (False, True):
+        stride = bf1.decode_plan_stride(w.ctx, w.b, w.L, dense)
+        plan = bf1.decode_plan(sl, table, num_pages, stride, w.b, w.L, dense)
+        ws = torch.empty(max(16, bf1.decode_workspace_size(w.batch, w.Hq, w.Hkv, w.d, stride)),
+                         dtype=torch.uint8, device="cuda")
+        step = lambda: bf1.attn_decode(q, kp, vp, sl, table, plan, w.b, out=o, lse=lse, workspace=ws)
+        mkplan = lambda: bf1.decode_plan(sl, table, num_pages, stride, w.b, w.L, dense, plan=plan)
+        step_graph = graph_ms(torch, step, 10)
+        plan_graph = graph_ms(torch, mkplan, 10)
+        step_eager = statistics.median(timed_reps(torch, step, 5, reps))
+        plan_eager = statistics.median(timed_reps(torch, mkplan, 5, reps))
+        torch.cuda.synchronize()
+        counts = plan[:, 1].cpu().tolist()
+        keys = sum((int(n) - 1) % w.b + 1 + w.b * int(c) for n, c in zip(sl.cpu().tolist(), counts))
+        nbytes = keys * w.Hkv * w.d * 2 * 2 + w.batch * w.Hq * w.d * 2 * 2 + w.batch * w.Hq * 4
+        key = "dense" if dense else "bf1"
+        rec[key] = {"step_us_graph": step_graph * 1e3, "step_us_eager": step_eager * 1e3,
+                    "plan_us_graph": plan_graph * 1e3, "plan_us_eager": plan_eager * 1e3,
+                    "pages_per_token": (sum(counts) + w.batch) / w.batch,
+                    "bytes_per_step": nbytes,
+                    "achieved_GBs": nbytes / (step_graph * 1e-3) / 1e9,
+                    "hbm_frac": nbytes / (step_graph * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                    "effective_us_plan_every_step": (step_graph + plan_graph) * 1e3,
+                    "effective_us_plan_per_epoch": (step_graph + plan_graph / w.b) * 1e3}
+        del ws, plan
+    rec["speedup_vs_dense_graph"] = rec["dense"]["step_us_graph"] / rec["bf1"]["step_us_graph"]
+    del q, kp, vp
+    torch.cuda.empty_cache()
+    return rec
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -358,6 +426,16 @@ def main():
         log("route variants: " + ", ".join(
             f"{kd} {vp[kd]['ms']:.4f} ms (depth {vp[kd]['max_shortest_path']})"
             for kd in ("bf1", "sliding", "static_random")))
+
+    if not args.no_decode:
+        rec["decode"] = []
+        for name, dw in synth.DECODE_WORKLOADS.items():
+            d = decode_point(torch, bf1, synth, dw, args.reps)
+            rec["decode"].append(d)
+            log(f"decode {name}: step {d['bf1']['step_us_graph']:.1f} us graph / "
+                f"{d['bf1']['step_us_eager']:.1f} us eager ({d['bf1']['achieved_GBs']:.0f} GB/s), plan "
+                f"{d['bf1']['plan_us_graph']:.1f} us; dense step {d['dense']['step_us_graph']:.1f} us "
+                f"({d['dense']['achieved_GBs']:.0f} GB/s); speedup {d['speedup_vs_dense_graph']:.2f}x")
 
     if args.sweep:
         os.makedirs(os.path.dirname(args.sweep_out), exist_ok=True)

@@ -207,6 +207,58 @@ int bf1_plan_variant(int32_t kind, int64_t n, int32_t B, int32_t L, uint64_t see
 int bf1_route_depth(const int32_t* row_ptr, const int32_t* col_idx, int32_t num_blocks,
                     int32_t* max_depth);
 
+/*
+ * One-token decode over a paged key/value cache (§3.2: a decoded token reads
+ * O(log NB) blocks; §4.2 "cached one-token decode"; §5.4 selected-page
+ * decode with a plan that persists across the route epoch).
+ *
+ * The newest token of sequence b sits at t = seq_lens[b] - 1 in query block
+ * j = t / B and attends to row t of the prefill mask: all keys of the earlier
+ * blocks of P(j) (Eq. 1) and keys j*B .. t of block j.  Its K and V must
+ * already be in the cache.  A cache page holds one block (B tokens):
+ *   K_pages, V_pages : [num_pages, Hkv, B, head_dim] bf16 (16-byte aligned)
+ *   page_table       : [batch, max_pages_per_seq] int32, logical block i of
+ *                      sequence b lives in page page_table[b, i]
+ *   seq_lens         : [batch] int32, >= 1
+ *   Q, O             : [batch, Hq, head_dim] bf16; LSE [batch, Hq] fp32
+ *                      (natural log, may be NULL)
+ * all device memory, caller-owned.
+ *
+ * Plan (built once per route epoch: it stays valid while every sequence's
+ * newest token remains in the block it was built for, i.e. for up to B
+ * steps):  int32 [batch, plan_stride] device memory, row b =
+ *   [j, c, the c physical pages of the earlier selected blocks (ascending
+ *    logical block), padding]
+ * bf1_decode_plan_stride gives the stride for sequences of up to
+ * max_seq_len tokens; `dense` = 1 plans every earlier block instead of P(j)
+ * (the dense decode comparator).  bf1_decode_plan is one kernel on `stream`;
+ * a sequence whose length is < 1, whose block is past max_pages_per_seq, or
+ * whose pages (earlier or self) fall outside [0, num_pages) is marked
+ * unplannable (j = -1).
+ *
+ * bf1_decode_attn: two kernels on `stream` (a split kernel over the pages and
+ * a merge of the split results, in a fixed order: deterministic).  A sequence
+ * whose plan row was made for another block (stale) or is unplannable gets
+ * NaN in its O rows and LSE; a plan row that bf1_decode_plan did not write
+ * gives undefined values, never a read outside the plan row and the cache.
+ * Keys past t in the self page are masked exactly, whatever the page holds.
+ * workspace: device scratch of at least bf1_decode_workspace_size() bytes,
+ * 16-byte aligned, contents irrelevant.  Supported: head_dim in {64, 128},
+ * B in {64, 128}, Hq / Hkv in {1, 2, 4, 8}, L <= 32.
+ */
+int bf1_decode_plan_stride(int64_t max_seq_len, int32_t B, int32_t L, int32_t dense,
+                           int32_t* plan_stride);
+int bf1_decode_plan(int32_t batch, const int32_t* seq_lens, const int32_t* page_table,
+                    int32_t max_pages_per_seq, int32_t num_pages, int32_t B, int32_t L, int32_t dense,
+                    int32_t* plan, int32_t plan_stride, void* stream);
+int bf1_decode_workspace_size(int32_t batch, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                              int32_t plan_stride, int64_t* bytes);
+int bf1_decode_attn(const void* Q, const void* K_pages, const void* V_pages, const int32_t* seq_lens,
+                    const int32_t* page_table, int32_t max_pages_per_seq, int32_t num_pages,
+                    const int32_t* plan, int32_t plan_stride, void* O, float* LSE, int32_t batch,
+                    int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t B, void* workspace,
+                    int64_t workspace_bytes, void* stream);
+
 /* Frees every cached plan (device memory owned by the library).  Must not
  * race with in-flight bf1_attn_fwd / bf1_attn_bwd calls that use those plans. */
 void bf1_release_plans(void);

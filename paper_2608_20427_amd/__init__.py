@@ -83,6 +83,15 @@ def load():
     lib.bf1_plan_variant.argtypes = [i32, i64, i32, i32, ctypes.c_uint64, vp, vp, i64]
     lib.bf1_route_depth.restype = ctypes.c_int
     lib.bf1_route_depth.argtypes = [vp, vp, i32, ctypes.POINTER(i32)]
+    lib.bf1_decode_plan_stride.restype = ctypes.c_int
+    lib.bf1_decode_plan_stride.argtypes = [i64, i32, i32, i32, ctypes.POINTER(i32)]
+    lib.bf1_decode_plan.restype = ctypes.c_int
+    lib.bf1_decode_plan.argtypes = [i32, vp, vp, i32, i32, i32, i32, i32, vp, i32, vp]
+    lib.bf1_decode_workspace_size.restype = ctypes.c_int
+    lib.bf1_decode_workspace_size.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(i64)]
+    lib.bf1_decode_attn.restype = ctypes.c_int
+    lib.bf1_decode_attn.argtypes = [vp, vp, vp, vp, vp, i32, i32, vp, i32, vp, vp, i32, i32, i32, i32,
+                                    i32, vp, i64, vp]
     _LIB = lib
     return lib
 
@@ -288,3 +297,79 @@ def attn_bwd(q, k, v, o, do, lse, B=64, L=2, dq=None, dk=None, dv=None, workspac
                                _ptr(workspace), workspace.numel(), _stream(stream)),
            "bf1_attn_bwd")
     return dq, dk, dv
+
+
+# ---- one-token decode over a paged cache ------------------------------------
+
+def decode_plan_stride(max_seq_len, B=64, L=2, dense=False):
+    """int32 entries per sequence of a decode plan for up to max_seq_len tokens."""
+    out = ctypes.c_int32(0)
+    _check(load().bf1_decode_plan_stride(int(max_seq_len), int(B), int(L), int(bool(dense)),
+                                         ctypes.byref(out)), "bf1_decode_plan_stride")
+    return out.value
+
+
+def _i32_cuda(t, name, dim):
+    import torch
+    if not t.is_cuda or t.dtype != torch.int32 or t.dim() != dim or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dim}-D int32 CUDA tensor")
+
+
+def decode_plan(seq_lens, page_table, num_pages, stride, B=64, L=2, dense=False, plan=None,
+                stream=None):
+    """Decode plan [batch, stride] int32 (device) for the current block of
+    every sequence: the pages of its earlier selected blocks."""
+    import torch
+    _i32_cuda(seq_lens, "seq_lens", 1)
+    _i32_cuda(page_table, "page_table", 2)
+    batch, max_pages = page_table.shape
+    if seq_lens.shape[0] != batch:
+        raise ValueError("seq_lens and page_table disagree on the batch size")
+    if plan is None:
+        plan = torch.empty((batch, stride), dtype=torch.int32, device=seq_lens.device)
+    elif plan.shape != (batch, stride) or plan.dtype != torch.int32 or not plan.is_contiguous():
+        raise ValueError("plan must be a contiguous int32 tensor [batch, stride]")
+    _check(load().bf1_decode_plan(batch, _ptr(seq_lens), _ptr(page_table), max_pages, int(num_pages),
+                                  int(B), int(L), int(bool(dense)), _ptr(plan), int(stride),
+                                  _stream(stream)), "bf1_decode_plan")
+    return plan
+
+
+def decode_workspace_size(batch, Hq, Hkv, head_dim, stride):
+    out = ctypes.c_int64(0)
+    _check(load().bf1_decode_workspace_size(int(batch), int(Hq), int(Hkv), int(head_dim), int(stride),
+                                            ctypes.byref(out)), "bf1_decode_workspace_size")
+    return out.value
+
+
+def attn_decode(q, k_pages, v_pages, seq_lens, page_table, plan, B=64, out=None, lse=None,
+                workspace=None, stream=None):
+    """Attention of each sequence's newest token over the paged cache, using
+    a decode plan; returns (O [batch, Hq, d] bf16, LSE [batch, Hq] fp32)."""
+    import torch
+    for name, t, dim in (("q", q, 3), ("k_pages", k_pages, 4), ("v_pages", v_pages, 4)):
+        if not t.is_cuda or t.dtype != torch.bfloat16 or t.dim() != dim or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {dim}-D bf16 CUDA tensor")
+    batch, Hq, d = q.shape
+    num_pages, Hkv, pw, dk = k_pages.shape
+    if v_pages.shape != k_pages.shape or dk != d or pw != B:
+        raise ValueError("k_pages / v_pages must be [num_pages, Hkv, B, d] matching q")
+    _i32_cuda(seq_lens, "seq_lens", 1)
+    _i32_cuda(page_table, "page_table", 2)
+    _i32_cuda(plan, "plan", 2)
+    if page_table.shape[0] != batch or seq_lens.shape[0] != batch or plan.shape[0] != batch:
+        raise ValueError("batch sizes disagree")
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((batch, Hq), dtype=torch.float32, device=q.device)
+    stride = plan.shape[1]
+    need = decode_workspace_size(batch, Hq, Hkv, d, stride)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    _check(load().bf1_decode_attn(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(seq_lens), _ptr(page_table),
+                                  page_table.shape[1], num_pages, _ptr(plan), stride, _ptr(out), _ptr(lse),
+                                  batch, Hq, Hkv, d, int(B), _ptr(workspace), workspace.numel(),
+                                  _stream(stream)), "bf1_decode_attn")
+    return out, lse
+

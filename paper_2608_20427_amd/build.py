@@ -45,14 +45,17 @@ def build(verbose=False, extra_hip_flags=()):
     os.makedirs(BUILD, exist_ok=True)
     k_obj = os.path.join(BUILD, "bf1_kernels.o")
     b_obj = os.path.join(BUILD, "bf1_bwd.o")
+    d_obj = os.path.join(BUILD, "bf1_decode.o")
     a_obj = os.path.join(BUILD, "bf1_api.o")
     _run([hipcc, *HIP_FLAGS, *extra_hip_flags, "-c", os.path.join(CSRC, "bf1_kernels.hip"),
           "-o", k_obj], verbose)
     _run([hipcc, *HIP_FLAGS, *extra_hip_flags, "-c", os.path.join(CSRC, "bf1_bwd.hip"),
           "-o", b_obj], verbose)
+    _run([hipcc, *HIP_FLAGS, *extra_hip_flags, "-c", os.path.join(CSRC, "bf1_decode.hip"),
+          "-o", d_obj], verbose)
     _run([gxx, *HOST_FLAGS, "-c", os.path.join(CSRC, "bf1_api.cpp"), "-o", a_obj], verbose)
     tmp = LIB + ".tmp"
-    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", k_obj, b_obj, a_obj, "-o", tmp,
+    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", k_obj, b_obj, d_obj, a_obj, "-o", tmp,
           f"-L{ROCM}/lib", "-lamdhip64", f"-Wl,-rpath,{ROCM}/lib"], verbose)
     os.replace(tmp, LIB)
     return LIB

@@ -55,6 +55,46 @@ struct BwdArgs {
 
 hipError_t launch_backward(const BwdArgs& a, hipStream_t stream);
 
+// One-token decode over a paged cache (validated arguments only).
+struct DecodePlanArgs {
+    int32_t batch;
+    const int32_t* seq_lens;    // [batch]
+    const int32_t* page_table;  // [batch, max_pages]
+    int32_t max_pages;
+    int32_t num_pages;
+    int32_t B;                  // page = block width
+    int32_t L;
+    int32_t dense;              // 1: every earlier block (dense comparator)
+    int32_t* plan;              // [batch, stride]
+    int32_t stride;
+    int32_t cap;                // stride - 2
+};
+hipError_t launch_decode_plan(const DecodePlanArgs& a, hipStream_t stream);
+
+struct DecodeArgs {
+    const void* Q;              // [batch, Hq, head_dim] bf16
+    const void* K;              // [num_pages, Hkv, B, head_dim] bf16
+    const void* V;
+    const int32_t* seq_lens;
+    const int32_t* page_table;
+    int32_t max_pages;
+    int32_t num_pages;
+    const int32_t* plan;
+    int32_t stride;
+    int32_t cap;
+    void* O;                    // [batch, Hq, head_dim] bf16
+    float* LSE;                 // [batch, Hq] or null
+    float* ws;                  // [batch * Hkv * nsplit, G * (head_dim + 2)] fp32
+    int32_t batch;
+    int32_t Hq;
+    int32_t Hkv;
+    int32_t head_dim;           // 64 or 128
+    int32_t B;                  // 64 or 128
+    int32_t nsplit;             // splits per (sequence, kv-head), <= 256
+    int32_t ppw;                // pages per split
+};
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+
 // Route planner: row_ptr[0..NB], col_idx[0..nnz) on `stream`.
 hipError_t launch_plan(int32_t NB, int32_t L, int32_t* row_ptr, int32_t* col_idx,
                        hipStream_t stream);

@@ -23,7 +23,9 @@ from dataclasses import dataclass, field, replace
 import numpy as np
 import torch
 
-__all__ = ["Workload", "WORKLOADS", "sweep", "make_qkv", "to_f64"]
+__all__ = ["Workload", "WORKLOADS", "sweep", "make_qkv", "to_f64", "DecodeWorkload",
+           "DECODE_WORKLOADS", "decode_seq_lens", "make_decode_host", "page_cache",
+           "make_decode_device"]
 
 
 @dataclass(frozen=True)
@@ -107,3 +109,112 @@ def make_grad_out(w, device="cpu"):
 def to_f64(t):
     """Exact float64 copy of a bf16 tensor as a NumPy array."""
     return t.detach().to("cpu").to(torch.float64).numpy()
+
+
+# ---------------------------------------------------------------------------
+# Decode: paged key/value caches
+# ---------------------------------------------------------------------------
+# The paper characterises one-token decode at contexts 32K and 64K for batch
+# 1, 8 and 32 in the same attention geometry (§5.4, Table 3).  A cache page
+# holds one block of b tokens of one sequence; pages are handed out in a
+# seeded random order (a fragmented pool, as a serving allocator leaves it),
+# and pages no sequence owns ("decoys") hold other values.
+
+@dataclass(frozen=True)
+class DecodeWorkload:
+    name: str
+    batch: int
+    ctx: int          # tokens in the cache of the longest sequence (newest included)
+    Hq: int
+    Hkv: int
+    d: int
+    b: int
+    L: int
+    seed: int
+    ragged: bool = False   # lengths uniform in [ctx/2, ctx] instead of all ctx
+    note: str = ""
+
+
+DECODE_WORKLOADS = {
+    f"decode_n{ctx}_batch{bt}": DecodeWorkload(f"decode_n{ctx}_batch{bt}", bt, ctx, 16, 8, 128, 64, 2,
+                                               4000 + bt + ctx // 1024,
+                                               note=f"Qwen3-0.6B geometry, {bt} sequences of {ctx} tokens")
+    for ctx in (32768, 65536) for bt in (1, 8, 32)
+}
+
+
+def decode_seq_lens(w):
+    """Sequence lengths (int32 numpy) of a decode workload."""
+    if not w.ragged:
+        return np.full(w.batch, w.ctx, dtype=np.int32)
+    rng = np.random.Generator(np.random.PCG64([w.seed, 2]))
+    return rng.integers(max(1, w.ctx // 2), w.ctx + 1, size=w.batch).astype(np.int32)
+
+
+def make_decode_host(w, seq_lens=None):
+    """Host draw for small decode cases: the newest token's query
+    [batch, Hq, d] and logical caches K, V [batch, Hkv, n_max, d] (bf16
+    torch tensors), n_max = the longest sequence; positions past a
+    sequence's length hold values it must never read."""
+    if seq_lens is None:
+        seq_lens = decode_seq_lens(w)
+    n_max = int(max(seq_lens))
+    rng = np.random.Generator(np.random.PCG64(w.seed))
+    q = rng.standard_normal((w.batch, w.Hq, w.d), dtype=np.float32)
+    k = rng.standard_normal((w.batch, w.Hkv, n_max, w.d), dtype=np.float32)
+    v = rng.standard_normal((w.batch, w.Hkv, n_max, w.d), dtype=np.float32)
+    return (torch.from_numpy(q).to(torch.bfloat16), torch.from_numpy(k).to(torch.bfloat16),
+            torch.from_numpy(v).to(torch.bfloat16), np.asarray(seq_lens, dtype=np.int32))
+
+
+def page_cache(k, v, seq_lens, b, seed, spare_pages=3, decoy=float("nan")):
+    """Scatter logical caches [batch, Hkv, n_max, d] into pages
+    [num_pages, Hkv, b, d] in a seeded random page order.  Returns
+    (k_pages, v_pages, page_table [batch, max_pages] int32, num_pages).
+    Page-table slots past a sequence's last block hold -1; spare pages and
+    the unused tail of each sequence's last page hold ``decoy``."""
+    batch, Hkv, n_max, d = k.shape
+    max_pages = -(-n_max // b)
+    owned = [-(-int(n) // b) for n in seq_lens]
+    num_pages = sum(owned) + spare_pages
+    rng = np.random.Generator(np.random.PCG64([seed, 3]))
+    order = rng.permutation(num_pages)
+    kp = torch.full((num_pages, Hkv, b, d), decoy, dtype=torch.bfloat16)
+    vp = torch.full((num_pages, Hkv, b, d), decoy, dtype=torch.bfloat16)
+    table = np.full((batch, max_pages), -1, dtype=np.int32)
+    nxt = 0
+    for beta in range(batch):
+        n = int(seq_lens[beta])
+        for i in range(owned[beta]):
+            page = int(order[nxt])
+            nxt += 1
+            table[beta, i] = page
+            lo, hi = i * b, min((i + 1) * b, n)
+            kp[page, :, : hi - lo] = k[beta, :, lo:hi]
+            vp[page, :, : hi - lo] = v[beta, :, lo:hi]
+    return kp, vp, torch.from_numpy(table), num_pages
+
+
+def make_decode_device(w, device="cuda"):
+    """Full-size decode inputs drawn on the device (a seeded torch generator;
+    the caches are gigabytes): q [batch, Hq, d], k_pages, v_pages
+    [num_pages, Hkv, b, d] bf16 standard normals, page_table [batch,
+    max_pages] int32 (a seeded random page order), seq_lens int32."""
+    seq_lens = decode_seq_lens(w)
+    max_pages = -(-w.ctx // w.b)
+    owned = [-(-int(n) // w.b) for n in seq_lens]
+    num_pages = sum(owned)
+    g = torch.Generator(device=device)
+    g.manual_seed(w.seed)
+    q = torch.randn((w.batch, w.Hq, w.d), generator=g, device=device, dtype=torch.float32).to(torch.bfloat16)
+    kp = torch.randn((num_pages, w.Hkv, w.b, w.d), generator=g, device=device, dtype=torch.bfloat16)
+    vp = torch.randn((num_pages, w.Hkv, w.b, w.d), generator=g, device=device, dtype=torch.bfloat16)
+    rng = np.random.Generator(np.random.PCG64([w.seed, 3]))
+    order = rng.permutation(num_pages).astype(np.int32)
+    table = np.full((w.batch, max_pages), -1, dtype=np.int32)
+    at = 0
+    for beta in range(w.batch):
+        table[beta, :owned[beta]] = order[at:at + owned[beta]]
+        at += owned[beta]
+    return (q, kp, vp, torch.from_numpy(seq_lens).to(device), torch.from_numpy(table).to(device),
+            num_pages)

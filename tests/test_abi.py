@@ -231,3 +231,55 @@ def test_route_depth_unreachable_and_invalid(lib):
     assert lib.bf1_plan_variant(1, 4096, 64, 2, 17, vp(r), vp(c), 441) == bf1.BF1_ERR_BUFFER_TOO_SMALL
     with pytest.raises(ValueError):
         bf1.plan_variant("dilated", 4096)
+
+
+# ---- decode (host-side checks) ------------------------------------------------
+
+def test_header_declares_the_decode():
+    names = declared_functions()
+    for want in ["bf1_decode_plan_stride", "bf1_decode_plan", "bf1_decode_workspace_size",
+                 "bf1_decode_attn"]:
+        assert want in names
+
+
+@pytest.mark.parametrize("n,B,L", [(1, 64, 2), (64, 64, 2), (65, 64, 2), (32768, 64, 2), (65536, 64, 2),
+                                   (30001, 64, 1), (5000, 128, 3), (1 << 20, 64, 0)])
+def test_decode_plan_stride_is_the_largest_route(lib, n, B, L):
+    NB = -(-n // B)
+    cap = max(len(orc.route(j, L)) - 1 for j in range(NB))
+    assert bf1.decode_plan_stride(n, B, L) == 2 + cap
+    assert bf1.decode_plan_stride(n, B, L, dense=True) == 2 + (NB - 1)
+
+
+def test_decode_workspace_size(lib):
+    # 32K, batch 1, Qwen geometry: P = 11 pages -> 11 splits of one page;
+    # record = G * (d + 2) floats per split
+    st = bf1.decode_plan_stride(32768, 64, 2)
+    assert st == 2 + 10
+    assert bf1.decode_workspace_size(1, 16, 8, 128, st) == (8 * 11 * 2 * 130 * 4 + 255) // 256 * 256
+    # batch 32: 2048 / 256 = 8 splits wanted -> 2 pages per split -> 6 splits
+    assert bf1.decode_workspace_size(32, 16, 8, 128, st) == (32 * 8 * 6 * 2 * 130 * 4 + 255) // 256 * 256
+
+
+def test_decode_invalid_arguments_rejected_without_device(lib):
+    fake = ctypes.c_void_p(1 << 20)
+    out = ctypes.c_int32(0)
+    assert lib.bf1_decode_plan_stride(0, 64, 2, 0, ctypes.byref(out)) == bf1.BF1_ERR_INVALID_ARG
+    assert lib.bf1_decode_plan_stride(100, 32, 2, 0, ctypes.byref(out)) == bf1.BF1_ERR_UNSUPPORTED
+    assert lib.bf1_decode_plan_stride(100, 64, 33, 0, ctypes.byref(out)) == bf1.BF1_ERR_INVALID_ARG
+    assert lib.bf1_decode_plan_stride(100, 64, 2, 2, ctypes.byref(out)) == bf1.BF1_ERR_INVALID_ARG
+    # plan: stride below 2, null pointers, batch 0 is a no-op
+    assert lib.bf1_decode_plan(1, fake, fake, 4, 4, 64, 2, 0, fake, 1, None) == bf1.BF1_ERR_INVALID_ARG
+    assert lib.bf1_decode_plan(1, None, fake, 4, 4, 64, 2, 0, fake, 20, None) == bf1.BF1_ERR_INVALID_ARG
+    assert lib.bf1_decode_plan(0, None, None, 4, 4, 64, 2, 0, None, 20, None) == bf1.BF1_OK
+    args = [fake] * 5
+    def attn(*tail, ws=fake, wsb=1 << 40, Hq=16, Hkv=8, d=128, B=64, stride=12):
+        return lib.bf1_decode_attn(*args, 4, 100, fake, stride, fake, None, 1, Hq, Hkv, d, B, ws, wsb, None)
+    assert attn(d=96) == bf1.BF1_ERR_UNSUPPORTED
+    assert attn(B=32) == bf1.BF1_ERR_UNSUPPORTED
+    assert attn(Hq=12, Hkv=8) == bf1.BF1_ERR_INVALID_ARG
+    assert attn(Hq=48, Hkv=3) == bf1.BF1_ERR_UNSUPPORTED
+    assert attn(stride=1) == bf1.BF1_ERR_INVALID_ARG
+    assert attn(ws=None) == bf1.BF1_ERR_INVALID_ARG
+    assert attn(ws=ctypes.c_void_p((1 << 20) + 8)) == bf1.BF1_ERR_INVALID_ARG
+    assert attn(wsb=1024) == bf1.BF1_ERR_BUFFER_TOO_SMALL
