@@ -275,7 +275,7 @@ def decode_point(torch, bf1, synth, w, reps):
         plan = bf1.decode_plan(sl, table, num_pages, stride, w.b, w.L, dense)
         ws = torch.empty(max(16, bf1.decode_workspace_size(w.batch, w.Hq, w.Hkv, w.d, stride)),
                          dtype=torch.uint8, device="cuda")
-        step = lambda: bf1.attn_decode(q, kp, vp, sl, table, plan, w.b, out=o, lse=lse, workspace=ws)
+        step = lambda: bf1.attn_decode(q, kp, vp, sl, plan, w.b, out=o, lse=lse, workspace=ws)
         mkplan = lambda: bf1.decode_plan(sl, table, num_pages, stride, w.b, w.L, dense, plan=plan)
         step_graph = graph_ms(torch, step, 10)
         plan_graph = graph_ms(torch, mkplan, 10)

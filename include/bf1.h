@@ -228,7 +228,9 @@ int bf1_route_depth(const int32_t* row_ptr, const int32_t* col_idx, int32_t num_
  * newest token remains in the block it was built for, i.e. for up to B
  * steps):  int32 [batch, plan_stride] device memory, row b =
  *   [j, c, the c physical pages of the earlier selected blocks (ascending
- *    logical block), padding]
+ *    logical block), the page of block j, padding]
+ * The page table is read only by the planner: a step reads its sequence
+ * length and its plan row.  Pages must not move while a plan is in use.
  * bf1_decode_plan_stride gives the stride for sequences of up to
  * max_seq_len tokens; `dense` = 1 plans every earlier block instead of P(j)
  * (the dense decode comparator).  bf1_decode_plan is one kernel on `stream`;
@@ -254,10 +256,9 @@ int bf1_decode_plan(int32_t batch, const int32_t* seq_lens, const int32_t* page_
 int bf1_decode_workspace_size(int32_t batch, int32_t Hq, int32_t Hkv, int32_t head_dim,
                               int32_t plan_stride, int64_t* bytes);
 int bf1_decode_attn(const void* Q, const void* K_pages, const void* V_pages, const int32_t* seq_lens,
-                    const int32_t* page_table, int32_t max_pages_per_seq, int32_t num_pages,
-                    const int32_t* plan, int32_t plan_stride, void* O, float* LSE, int32_t batch,
-                    int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t B, void* workspace,
-                    int64_t workspace_bytes, void* stream);
+                    int32_t num_pages, const int32_t* plan, int32_t plan_stride, void* O, float* LSE,
+                    int32_t batch, int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t B,
+                    void* workspace, int64_t workspace_bytes, void* stream);
 
 /* Frees every cached plan (device memory owned by the library).  Must not
  * race with in-flight bf1_attn_fwd / bf1_attn_bwd calls that use those plans. */

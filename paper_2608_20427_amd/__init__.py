@@ -90,8 +90,8 @@ def load():
     lib.bf1_decode_workspace_size.restype = ctypes.c_int
     lib.bf1_decode_workspace_size.argtypes = [i32, i32, i32, i32, i32, ctypes.POINTER(i64)]
     lib.bf1_decode_attn.restype = ctypes.c_int
-    lib.bf1_decode_attn.argtypes = [vp, vp, vp, vp, vp, i32, i32, vp, i32, vp, vp, i32, i32, i32, i32,
-                                    i32, vp, i64, vp]
+    lib.bf1_decode_attn.argtypes = [vp, vp, vp, vp, i32, vp, i32, vp, vp, i32, i32, i32, i32, i32, vp,
+                                    i64, vp]
     _LIB = lib
     return lib
 
@@ -342,8 +342,8 @@ def decode_workspace_size(batch, Hq, Hkv, head_dim, stride):
     return out.value
 
 
-def attn_decode(q, k_pages, v_pages, seq_lens, page_table, plan, B=64, out=None, lse=None,
-                workspace=None, stream=None):
+def attn_decode(q, k_pages, v_pages, seq_lens, plan, B=64, out=None, lse=None, workspace=None,
+                stream=None):
     """Attention of each sequence's newest token over the paged cache, using
     a decode plan; returns (O [batch, Hq, d] bf16, LSE [batch, Hq] fp32)."""
     import torch
@@ -355,9 +355,8 @@ def attn_decode(q, k_pages, v_pages, seq_lens, page_table, plan, B=64, out=None,
     if v_pages.shape != k_pages.shape or dk != d or pw != B:
         raise ValueError("k_pages / v_pages must be [num_pages, Hkv, B, d] matching q")
     _i32_cuda(seq_lens, "seq_lens", 1)
-    _i32_cuda(page_table, "page_table", 2)
     _i32_cuda(plan, "plan", 2)
-    if page_table.shape[0] != batch or seq_lens.shape[0] != batch or plan.shape[0] != batch:
+    if seq_lens.shape[0] != batch or plan.shape[0] != batch:
         raise ValueError("batch sizes disagree")
     if out is None:
         out = torch.empty_like(q)
@@ -367,9 +366,8 @@ def attn_decode(q, k_pages, v_pages, seq_lens, page_table, plan, B=64, out=None,
     need = decode_workspace_size(batch, Hq, Hkv, d, stride)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
-    _check(load().bf1_decode_attn(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(seq_lens), _ptr(page_table),
-                                  page_table.shape[1], num_pages, _ptr(plan), stride, _ptr(out), _ptr(lse),
-                                  batch, Hq, Hkv, d, int(B), _ptr(workspace), workspace.numel(),
-                                  _stream(stream)), "bf1_decode_attn")
+    _check(load().bf1_decode_attn(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(seq_lens), num_pages,
+                                  _ptr(plan), stride, _ptr(out), _ptr(lse), batch, Hq, Hkv, d, int(B),
+                                  _ptr(workspace), workspace.numel(), _stream(stream)), "bf1_decode_attn")
     return out, lse
 

@@ -80,11 +80,12 @@ bool decode_cap(int64_t max_seq_len, int64_t B, int64_t L, bool dense, int64_t* 
 }
 
 // Splits per (sequence, kv-head) and pages per split for lists of up to P
-// pages: enough workgroups to cover the chip (about 2048), at most 256
+// pages: about 1024 workgroups (four per CU; more or fewer measured no
+// faster for the selected lists and slower for long dense ones), at most 256
 // splits, splits as even as possible.
 void decode_splits(int64_t batch, int64_t Hkv, int64_t P, int32_t* nsplit, int32_t* ppw) {
     const int64_t units = std::max<int64_t>(1, batch * Hkv);
-    const int64_t want = std::max<int64_t>(1, (2048 + units - 1) / units);
+    const int64_t want = std::max<int64_t>(1, (1024 + units - 1) / units);
     int64_t ns = std::min<int64_t>(std::min<int64_t>(P, want), 256);
     ns = std::max<int64_t>(ns, 1);
     const int64_t pp = (P + ns - 1) / ns;
@@ -499,7 +500,7 @@ int bf1_decode_plan_stride(int64_t max_seq_len, int32_t B, int32_t L, int32_t de
     if (max_seq_len >= (int64_t(1) << 31)) return BF1_ERR_INVALID_ARG;
     int64_t cap;
     if (!decode_cap(max_seq_len, B, L, dense != 0, &cap)) return BF1_ERR_INVALID_ARG;
-    *stride = (int32_t)(2 + cap);
+    *stride = (int32_t)(3 + cap);
     return BF1_OK;
 }
 
@@ -508,33 +509,32 @@ int bf1_decode_plan(int32_t batch, const int32_t* seq_lens, const int32_t* page_
                     int32_t* plan, int32_t plan_stride, void* stream) {
     if (batch < 0 || L < 0 || L > 32 || (dense != 0 && dense != 1)) return BF1_ERR_INVALID_ARG;
     if (B != 64 && B != 128) return BF1_ERR_UNSUPPORTED;
-    if (max_pages_per_seq < 1 || num_pages < 1 || plan_stride < 2) return BF1_ERR_INVALID_ARG;
+    if (max_pages_per_seq < 1 || num_pages < 1 || plan_stride < 3) return BF1_ERR_INVALID_ARG;
     if (batch == 0) return BF1_OK;
     if (!seq_lens || !page_table || !plan) return BF1_ERR_INVALID_ARG;
     if (!aligned(seq_lens, 4) || !aligned(page_table, 4) || !aligned(plan, 4)) return BF1_ERR_INVALID_ARG;
     bf1::DecodePlanArgs a{batch, seq_lens, page_table, max_pages_per_seq, num_pages, B, L, dense,
-                          plan, plan_stride, plan_stride - 2};
+                          plan, plan_stride, plan_stride - 3};
     return status_of(bf1::launch_decode_plan(a, (hipStream_t)stream));
 }
 
 int bf1_decode_workspace_size(int32_t batch, int32_t Hq, int32_t Hkv, int32_t head_dim,
                               int32_t plan_stride, int64_t* bytes) {
-    if (!bytes || batch < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || plan_stride < 2)
+    if (!bytes || batch < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || plan_stride < 3)
         return BF1_ERR_INVALID_ARG;
     if (head_dim != 64 && head_dim != 128) return BF1_ERR_UNSUPPORTED;
     int32_t nsplit, ppw;
-    decode_splits(batch, Hkv, (int64_t)plan_stride - 1, &nsplit, &ppw);
+    decode_splits(batch, Hkv, (int64_t)plan_stride - 2, &nsplit, &ppw);
     *bytes = decode_ws_bytes(batch, Hq, Hkv, head_dim, nsplit);
     return BF1_OK;
 }
 
 int bf1_decode_attn(const void* Q, const void* K_pages, const void* V_pages, const int32_t* seq_lens,
-                    const int32_t* page_table, int32_t max_pages_per_seq, int32_t num_pages,
-                    const int32_t* plan, int32_t plan_stride, void* O, float* LSE, int32_t batch,
-                    int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t B, void* workspace,
-                    int64_t workspace_bytes, void* stream) {
+                    int32_t num_pages, const int32_t* plan, int32_t plan_stride, void* O, float* LSE,
+                    int32_t batch, int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t B,
+                    void* workspace, int64_t workspace_bytes, void* stream) {
     if (batch < 0 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return BF1_ERR_INVALID_ARG;
-    if (max_pages_per_seq < 1 || num_pages < 1 || plan_stride < 2) return BF1_ERR_INVALID_ARG;
+    if (num_pages < 1 || plan_stride < 3) return BF1_ERR_INVALID_ARG;
     const int32_t G = Hq / Hkv;
     if (head_dim != 64 && head_dim != 128) return BF1_ERR_UNSUPPORTED;
     if (B != 64 && B != 128) return BF1_ERR_UNSUPPORTED;
@@ -542,18 +542,16 @@ int bf1_decode_attn(const void* Q, const void* K_pages, const void* V_pages, con
     if ((int64_t)batch * Hkv > (int64_t(1) << 22)) return BF1_ERR_INVALID_ARG;
     if ((double)num_pages * Hkv * B * head_dim > 4.0e18) return BF1_ERR_INVALID_ARG;
     if (batch == 0) return BF1_OK;
-    if (!Q || !K_pages || !V_pages || !seq_lens || !page_table || !plan || !O || !workspace)
-        return BF1_ERR_INVALID_ARG;
+    if (!Q || !K_pages || !V_pages || !seq_lens || !plan || !O || !workspace) return BF1_ERR_INVALID_ARG;
     if (!aligned(Q, 16) || !aligned(K_pages, 16) || !aligned(V_pages, 16) || !aligned(O, 16) ||
-        !aligned(workspace, 16) || !aligned(seq_lens, 4) || !aligned(page_table, 4) || !aligned(plan, 4))
+        !aligned(workspace, 16) || !aligned(seq_lens, 4) || !aligned(plan, 4))
         return BF1_ERR_INVALID_ARG;
     if (LSE && !aligned(LSE, 4)) return BF1_ERR_INVALID_ARG;
     int32_t nsplit, ppw;
-    decode_splits(batch, Hkv, (int64_t)plan_stride - 1, &nsplit, &ppw);
+    decode_splits(batch, Hkv, (int64_t)plan_stride - 2, &nsplit, &ppw);
     if (workspace_bytes < decode_ws_bytes(batch, Hq, Hkv, head_dim, nsplit)) return BF1_ERR_BUFFER_TOO_SMALL;
-    bf1::DecodeArgs a{Q, K_pages, V_pages, seq_lens, page_table, max_pages_per_seq, num_pages, plan,
-                      plan_stride, plan_stride - 2, O, LSE, (float*)workspace, batch, Hq, Hkv,
-                      head_dim, B, nsplit, ppw};
+    bf1::DecodeArgs a{Q, K_pages, V_pages, seq_lens, num_pages, plan, plan_stride, plan_stride - 3, O,
+                      LSE, (float*)workspace, batch, Hq, Hkv, head_dim, B, nsplit, ppw};
     return status_of(bf1::launch_decode(a, (hipStream_t)stream));
 }
 

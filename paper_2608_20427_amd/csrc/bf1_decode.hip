@@ -12,12 +12,15 @@
 // Cache layout: K and V pages [num_pages, Hkv, B, D] bf16 (a page holds B
 // consecutive tokens of one sequence; one (page, kv-head) slice is contiguous,
 // B * D * 2 bytes).  A page table [batch, max_pages] maps each sequence's
-// logical block i to its physical page.
+// logical block i to its physical page; only the planner reads it.
 //
-// Plan row of a sequence (int32, `stride` = 2 + cap entries):
+// Plan row of a sequence (int32, `stride` = 3 + cap entries):
 //   [0]                 block j the plan was made for (-1: not plannable)
 //   [1]                 c, the number of earlier selected pages
 //   [2, 2 + c)          their physical pages, ascending logical block
+//   [2 + c]             the page of block j itself
+// A step reads only its sequence length and this row, two independent loads,
+// before it can address the cache.
 //
 // Split kernel: one workgroup of four waves per (sequence, kv-head, split);
 // a split is `ppw` consecutive pages of the sequence's list (earlier pages,
@@ -97,6 +100,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void decode_plan_kernel(
         if (tid == 0) {
             const int32_t p = pt[j];  // the self page must exist as well
             if (p < 0 || p >= num_pages) atomicOr(&bad, 1);
+            row[2 + c] = p;
         }
     }
     __syncthreads();
@@ -118,27 +122,24 @@ __device__ __forceinline__ void bf16x8_to_float(u32x4 w, float* f) {
 // Decode attention.
 // ---------------------------------------------------------------------------
 
-// What one step of sequence b reads: its newest position t, block j, the
-// number c of earlier pages in its plan row and its self page.  False if the
-// plan row was made for another block, is not a planner row, or the self page
-// is missing; both kernels take the same decision from the same data.
+// What one step of sequence b reads: its newest position t, block j and the
+// number c of earlier pages in its plan row.  False if the plan row was made
+// for another block or is not a planner row; both kernels take the same
+// decision from the same data.
 struct StepView {
     int64_t t, j;
     int c;
-    int32_t selfpage;
 };
 
-__device__ __forceinline__ bool step_view(const int32_t* __restrict__ seq_lens,
-                                          const int32_t* __restrict__ page_table, int32_t max_pages,
-                                          int32_t num_pages, const int32_t* row, int32_t cap, int PW,
-                                          int b, StepView* v) {
-    v->t = (int64_t)seq_lens[b] - 1;
+__device__ __forceinline__ bool step_view(const int32_t* __restrict__ seq_lens, const int32_t* row,
+                                          int32_t cap, int PW, int b, StepView* v) {
+    const int32_t n = seq_lens[b];
+    const int32_t pj = row[0];
+    const int32_t pc = row[1];
+    v->t = (int64_t)n - 1;
     v->j = v->t >= 0 ? v->t / PW : -1;
-    if (v->t < 0 || v->j >= max_pages || row[0] != v->j) return false;
-    v->c = row[1];
-    if (v->c < 0 || v->c > cap) return false;
-    v->selfpage = page_table[(int64_t)b * max_pages + v->j];
-    return v->selfpage >= 0 && v->selfpage < num_pages;
+    v->c = pc;
+    return v->t >= 0 && pj == v->j && pc >= 0 && pc <= cap;
 }
 
 template <int D, int G>
@@ -151,10 +152,9 @@ __device__ __forceinline__ void write_nan(__bf16* O, float* LSE, int b, int Hq, 
 template <int D, int G, int PW>
 __global__ __launch_bounds__(DEC_THREADS) void decode_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ Kp, const __bf16* __restrict__ Vp,
-    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ page_table, int32_t max_pages,
-    int32_t num_pages, const int32_t* __restrict__ plan, int32_t stride, int32_t cap,
-    __bf16* __restrict__ O, float* __restrict__ LSE, float* __restrict__ ws, int32_t Hkv,
-    int32_t nsplit, int32_t ppw, float c_log2) {
+    const int32_t* __restrict__ seq_lens, int32_t num_pages, const int32_t* __restrict__ plan,
+    int32_t stride, int32_t cap, __bf16* __restrict__ O, float* __restrict__ LSE,
+    float* __restrict__ ws, int32_t Hkv, int32_t nsplit, int32_t ppw, float c_log2) {
     constexpr int LPR = D / 8;            // lanes per key row (16 bytes each)
     constexpr int RPI = 64 / LPR;         // key rows per wave-wide load
     constexpr int KPW = PW / DEC_WAVES;   // keys of a page per wave
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_kernel(
     const int32_t* row = plan + (int64_t)b * stride;
 
     StepView sv;
-    if (!step_view(seq_lens, page_table, max_pages, num_pages, row, cap, PW, b, &sv)) {
+    if (!step_view(seq_lens, row, cap, PW, b, &sv)) {
         // stale or unplannable: the outputs of this (sequence, kv-head) are NaN
         if (s == 0) write_nan<D, G>(O, LSE, b, Hq, h, tid);
         return;
@@ -214,7 +214,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_kernel(
     auto load_page = [&](int p, u32x4* kr, u32x4* vr) {
         // pages written by the planner are in range; the clamp only keeps a
         // foreign plan row from addressing memory outside the cache
-        const int32_t page = p < c ? min(max(row[2 + p], 0), num_pages - 1) : sv.selfpage;
+        const int32_t page = min(max(row[2 + p], 0), num_pages - 1);
         const int64_t base = ((int64_t)page * Hkv + h) * PW * D;
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
@@ -348,10 +348,9 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_kernel(
 // of eight (their loads issued together) into a running max / sum / row.
 template <int D, int G, int PW>
 __global__ __launch_bounds__(DEC_THREADS) void decode_merge_kernel(
-    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ page_table, int32_t max_pages,
-    int32_t num_pages, const int32_t* __restrict__ plan, int32_t stride, int32_t cap,
-    __bf16* __restrict__ O, float* __restrict__ LSE, const float* __restrict__ ws, int32_t Hkv,
-    int32_t nsplit, int32_t ppw) {
+    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ plan, int32_t stride,
+    int32_t cap, __bf16* __restrict__ O, float* __restrict__ LSE, const float* __restrict__ ws,
+    int32_t Hkv, int32_t nsplit, int32_t ppw) {
     constexpr int REC = G * (D + 2);
     constexpr int U = 8;
     const int tid = threadIdx.x;
@@ -360,7 +359,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_merge_kernel(
     const int b = bh / Hkv;
     const int Hq = Hkv * G;
     StepView sv;
-    if (!step_view(seq_lens, page_table, max_pages, num_pages, plan + (int64_t)b * stride, cap, PW, b, &sv))
+    if (!step_view(seq_lens, plan + (int64_t)b * stride, cap, PW, b, &sv))
         return;  // the split kernel wrote NaN
     const int nsb = (sv.c + 1 + ppw - 1) / ppw;
     if (nsb <= 1) return;  // the split kernel wrote the result
@@ -403,13 +402,13 @@ hipError_t launch_decode_pw(const DecodeArgs& a, hipStream_t st) {
     const float c_log2 = LOG2E / sqrtf((float)D);
     hipLaunchKernelGGL((decode_kernel<D, G, PW>), dim3((unsigned)((int64_t)a.batch * a.Hkv * a.nsplit)),
                        dim3(DEC_THREADS), 0, st, (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
-                       a.seq_lens, a.page_table, a.max_pages, a.num_pages, a.plan, a.stride, a.cap,
-                       (__bf16*)a.O, a.LSE, a.ws, a.Hkv, a.nsplit, a.ppw, c_log2);
+                       a.seq_lens, a.num_pages, a.plan, a.stride, a.cap, (__bf16*)a.O, a.LSE, a.ws, a.Hkv,
+                       a.nsplit, a.ppw, c_log2);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.nsplit <= 1) return e;
     hipLaunchKernelGGL((decode_merge_kernel<D, G, PW>), dim3((unsigned)((int64_t)a.batch * a.Hkv)),
-                       dim3(DEC_THREADS), 0, st, a.seq_lens, a.page_table, a.max_pages, a.num_pages, a.plan,
-                       a.stride, a.cap, (__bf16*)a.O, a.LSE, a.ws, a.Hkv, a.nsplit, a.ppw);
+                       dim3(DEC_THREADS), 0, st, a.seq_lens, a.plan, a.stride, a.cap, (__bf16*)a.O, a.LSE,
+                       a.ws, a.Hkv, a.nsplit, a.ppw);
     return hipGetLastError();
 }
 

@@ -67,7 +67,7 @@ struct DecodePlanArgs {
     int32_t dense;              // 1: every earlier block (dense comparator)
     int32_t* plan;              // [batch, stride]
     int32_t stride;
-    int32_t cap;                // stride - 2
+    int32_t cap;                // stride - 3
 };
 hipError_t launch_decode_plan(const DecodePlanArgs& a, hipStream_t stream);
 
@@ -76,8 +76,6 @@ struct DecodeArgs {
     const void* K;              // [num_pages, Hkv, B, head_dim] bf16
     const void* V;
     const int32_t* seq_lens;
-    const int32_t* page_table;
-    int32_t max_pages;
     int32_t num_pages;
     const int32_t* plan;
     int32_t stride;

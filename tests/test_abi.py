@@ -247,18 +247,18 @@ def test_header_declares_the_decode():
 def test_decode_plan_stride_is_the_largest_route(lib, n, B, L):
     NB = -(-n // B)
     cap = max(len(orc.route(j, L)) - 1 for j in range(NB))
-    assert bf1.decode_plan_stride(n, B, L) == 2 + cap
-    assert bf1.decode_plan_stride(n, B, L, dense=True) == 2 + (NB - 1)
+    assert bf1.decode_plan_stride(n, B, L) == 3 + cap
+    assert bf1.decode_plan_stride(n, B, L, dense=True) == 3 + (NB - 1)
 
 
 def test_decode_workspace_size(lib):
     # 32K, batch 1, Qwen geometry: P = 11 pages -> 11 splits of one page;
     # record = G * (d + 2) floats per split
     st = bf1.decode_plan_stride(32768, 64, 2)
-    assert st == 2 + 10
+    assert st == 3 + 10
     assert bf1.decode_workspace_size(1, 16, 8, 128, st) == (8 * 11 * 2 * 130 * 4 + 255) // 256 * 256
-    # batch 32: 2048 / 256 = 8 splits wanted -> 2 pages per split -> 6 splits
-    assert bf1.decode_workspace_size(32, 16, 8, 128, st) == (32 * 8 * 6 * 2 * 130 * 4 + 255) // 256 * 256
+    # batch 32: 1024 / 256 = 4 splits wanted -> 3 pages per split -> 4 splits
+    assert bf1.decode_workspace_size(32, 16, 8, 128, st) == (32 * 8 * 4 * 2 * 130 * 4 + 255) // 256 * 256
 
 
 def test_decode_invalid_arguments_rejected_without_device(lib):
@@ -269,17 +269,17 @@ def test_decode_invalid_arguments_rejected_without_device(lib):
     assert lib.bf1_decode_plan_stride(100, 64, 33, 0, ctypes.byref(out)) == bf1.BF1_ERR_INVALID_ARG
     assert lib.bf1_decode_plan_stride(100, 64, 2, 2, ctypes.byref(out)) == bf1.BF1_ERR_INVALID_ARG
     # plan: stride below 2, null pointers, batch 0 is a no-op
-    assert lib.bf1_decode_plan(1, fake, fake, 4, 4, 64, 2, 0, fake, 1, None) == bf1.BF1_ERR_INVALID_ARG
+    assert lib.bf1_decode_plan(1, fake, fake, 4, 4, 64, 2, 0, fake, 2, None) == bf1.BF1_ERR_INVALID_ARG
     assert lib.bf1_decode_plan(1, None, fake, 4, 4, 64, 2, 0, fake, 20, None) == bf1.BF1_ERR_INVALID_ARG
     assert lib.bf1_decode_plan(0, None, None, 4, 4, 64, 2, 0, None, 20, None) == bf1.BF1_OK
-    args = [fake] * 5
-    def attn(*tail, ws=fake, wsb=1 << 40, Hq=16, Hkv=8, d=128, B=64, stride=12):
-        return lib.bf1_decode_attn(*args, 4, 100, fake, stride, fake, None, 1, Hq, Hkv, d, B, ws, wsb, None)
+    args = [fake] * 4
+    def attn(*tail, ws=fake, wsb=1 << 40, Hq=16, Hkv=8, d=128, B=64, stride=13):
+        return lib.bf1_decode_attn(*args, 100, fake, stride, fake, None, 1, Hq, Hkv, d, B, ws, wsb, None)
     assert attn(d=96) == bf1.BF1_ERR_UNSUPPORTED
     assert attn(B=32) == bf1.BF1_ERR_UNSUPPORTED
     assert attn(Hq=12, Hkv=8) == bf1.BF1_ERR_INVALID_ARG
     assert attn(Hq=48, Hkv=3) == bf1.BF1_ERR_UNSUPPORTED
-    assert attn(stride=1) == bf1.BF1_ERR_INVALID_ARG
+    assert attn(stride=2) == bf1.BF1_ERR_INVALID_ARG
     assert attn(ws=None) == bf1.BF1_ERR_INVALID_ARG
     assert attn(ws=ctypes.c_void_p((1 << 20) + 8)) == bf1.BF1_ERR_INVALID_ARG
     assert attn(wsb=1024) == bf1.BF1_ERR_BUFFER_TOO_SMALL

@@ -60,7 +60,7 @@ def setup_case(w, seq_lens, spare=3, decoy=float("nan"), dense=False, page_seed=
 def run_decode(w, dev, dense=False, plan=None):
     if plan is None:
         plan = bf1.decode_plan(dev["sl"], dev["table"], dev["num_pages"], dev["stride"], w.b, w.L, dense)
-    o, l = bf1.attn_decode(dev["q"], dev["kp"], dev["vp"], dev["sl"], dev["table"], plan, w.b)
+    o, l = bf1.attn_decode(dev["q"], dev["kp"], dev["vp"], dev["sl"], plan, w.b)
     torch.cuda.synchronize()
     return o, l, plan
 
@@ -85,6 +85,7 @@ def test_decode_plan_bit_exact(B, L, dense):
         j, earlier = orc.decode_plan(int(sl[beta]), table[beta], B, L, dense)
         assert plan[beta, 0] == j and plan[beta, 1] == len(earlier), beta
         assert plan[beta, 2:2 + len(earlier)].tolist() == earlier, beta
+        assert plan[beta, 2 + len(earlier)] == table[beta, j], beta
 
 
 def test_decode_plan_marks_unplannable_rows():
@@ -97,7 +98,7 @@ def test_decode_plan_marks_unplannable_rows():
     plan = bf1.decode_plan(torch.from_numpy(sl).cuda(), torch.from_numpy(table).cuda(), 50, stride, B,
                            L).cpu().numpy()
     assert plan[:, 0].tolist() == [-1, 1, -1, -1, -1]
-    assert plan[1, 1] == 1 and plan[1, 2] == table[1, 0]
+    assert plan[1, 1] == 1 and plan[1, 2] == table[1, 0] and plan[1, 3] == table[1, 1]
 
 
 # ---------------------------------------------------------------------------
@@ -152,7 +153,7 @@ def test_decode_matches_gpu_forward_last_row():
         stride = bf1.decode_plan_stride(n, 64, 2)
         plan = bf1.decode_plan(torch.from_numpy(sl).cuda(), table.cuda(), num_pages, stride, 64, 2)
         qd = q[:, :, n - 1].contiguous()
-        o, l = bf1.attn_decode(qd, kp.cuda(), vp.cuda(), torch.from_numpy(sl).cuda(), table.cuda(), plan, 64)
+        o, l = bf1.attn_decode(qd, kp.cuda(), vp.cuda(), torch.from_numpy(sl).cuda(), plan, 64)
         torch.cuda.synchronize()
         err = (o.float() - of[:, :, n - 1].float()).abs().max().item()
         lerr = (l - lf[:, :, n - 1]).abs().max().item()
@@ -187,20 +188,20 @@ def test_persistent_plan_across_the_epoch_and_stale_detection():
     qf, kf, vf = synth.to_f64(q), synth.to_f64(k), synth.to_f64(v)
     for step in (0, 1, 31, 59):
         sl = start + step
-        o, l = bf1.attn_decode(q.cuda(), kp, vp, torch.from_numpy(sl).cuda(), table, plan, 64)
+        o, l = bf1.attn_decode(q.cuda(), kp, vp, torch.from_numpy(sl).cuda(), plan, 64)
         torch.cuda.synchronize()
         o_ref, l_ref = orc.attn_decode_fp64(qf, kf, vf, sl, 64, 2)
         compare(o, l, o_ref, l_ref, f"step {step}")
     # sequence 1 crosses into block 11 at length 705; sequence 0 stays in block 16
     sl = np.array([1024 + 64, 705], dtype=np.int32)
-    o, l = bf1.attn_decode(q.cuda(), kp, vp, torch.from_numpy(sl).cuda(), table, plan, 64)
+    o, l = bf1.attn_decode(q.cuda(), kp, vp, torch.from_numpy(sl).cuda(), plan, 64)
     torch.cuda.synchronize()
     assert torch.isnan(o[1].float()).all() and torch.isnan(l[1]).all()
     o_ref, l_ref = orc.attn_decode_fp64(qf, kf, vf, sl, 64, 2)
     compare(o, l, o_ref, l_ref, "stale row isolated", rows=[0])
     # re-planning fixes it
     plan = bf1.decode_plan(torch.from_numpy(sl).cuda(), table, num_pages, stride, 64, 2)
-    o, l = bf1.attn_decode(q.cuda(), kp, vp, torch.from_numpy(sl).cuda(), table, plan, 64)
+    o, l = bf1.attn_decode(q.cuda(), kp, vp, torch.from_numpy(sl).cuda(), plan, 64)
     torch.cuda.synchronize()
     compare(o, l, o_ref, l_ref, "replanned")
 
@@ -227,7 +228,7 @@ def test_decode_full_size_sampled(name):
     q, kp, vp, sl, table, num_pages = synth.make_decode_device(w)
     stride = bf1.decode_plan_stride(w.ctx, w.b, w.L)
     plan = bf1.decode_plan(sl, table, num_pages, stride, w.b, w.L)
-    o, l = bf1.attn_decode(q, kp, vp, sl, table, plan, w.b)
+    o, l = bf1.attn_decode(q, kp, vp, sl, plan, w.b)
     torch.cuda.synchronize()
     for beta in sorted({0, w.batch - 1}):
         n = int(sl[beta])
@@ -246,16 +247,15 @@ def test_decode_workspace_too_small_and_lse_optional():
     need = bf1.decode_workspace_size(2, 4, 2, 128, dev["stride"])
     ws = torch.empty(need - 256, dtype=torch.uint8, device="cuda")
     with pytest.raises(bf1.BF1Error) as e:
-        bf1.attn_decode(dev["q"], dev["kp"], dev["vp"], dev["sl"], dev["table"], plan, 64, workspace=ws)
+        bf1.attn_decode(dev["q"], dev["kp"], dev["vp"], dev["sl"], plan, 64, workspace=ws)
     assert e.value.status == bf1.BF1_ERR_BUFFER_TOO_SMALL
     o1, l1, _ = run_decode(w, dev, plan=plan)
     lib = bf1.load()
     o2 = torch.empty_like(o1)
     ws = torch.empty(need, dtype=torch.uint8, device="cuda")
     st = lib.bf1_decode_attn(bf1._ptr(dev["q"]), bf1._ptr(dev["kp"]), bf1._ptr(dev["vp"]), bf1._ptr(dev["sl"]),
-                             bf1._ptr(dev["table"]), dev["table"].shape[1], dev["num_pages"], bf1._ptr(plan),
-                             dev["stride"], bf1._ptr(o2), None, 2, 4, 2, 128, 64, bf1._ptr(ws), need,
-                             bf1._stream(None))
+                             dev["num_pages"], bf1._ptr(plan), dev["stride"], bf1._ptr(o2), None, 2, 4, 2, 128,
+                             64, bf1._ptr(ws), need, bf1._stream(None))
     torch.cuda.synchronize()
     assert st == bf1.BF1_OK and torch.equal(o1, o2)
 
@@ -273,8 +273,7 @@ def test_decode_step_replays_in_a_graph():
 
     def step():
         bf1.decode_plan(dev["sl"], dev["table"], dev["num_pages"], dev["stride"], w.b, w.L, plan=plan)
-        bf1.attn_decode(dev["q"], dev["kp"], dev["vp"], dev["sl"], dev["table"], plan, w.b, out=o, lse=l,
-                        workspace=ws)
+        bf1.attn_decode(dev["q"], dev["kp"], dev["vp"], dev["sl"], plan, w.b, out=o, lse=l, workspace=ws)
 
     step()
     torch.cuda.synchronize()
