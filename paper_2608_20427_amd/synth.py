@@ -25,7 +25,7 @@ import torch
 
 __all__ = ["Workload", "WORKLOADS", "sweep", "make_qkv", "to_f64", "DecodeWorkload",
            "DECODE_WORKLOADS", "decode_seq_lens", "make_decode_host", "page_cache",
-           "make_decode_device"]
+           "make_decode_device", "ModelConfig", "QWEN3_06B", "make_model_weights", "make_tokens"]
 
 
 @dataclass(frozen=True)
@@ -218,3 +218,79 @@ def make_decode_device(w, device="cuda"):
         at += owned[beta]
     return (q, kp, vp, torch.from_numpy(seq_lens).to(device), torch.from_numpy(table).to(device),
             num_pages)
+
+
+# ---------------------------------------------------------------------------
+# Whole-model prefill timing: a decoder stack of the evaluated geometry
+# ---------------------------------------------------------------------------
+# The paper times whole-model prefill (time to first token) of Qwen3-0.6B with
+# 8 or all 28 attention layers on the BF1 route (§4.3, §5.3).  The trained
+# weights are not available here, so the stack gets seeded random weights of
+# the published Qwen3-0.6B shapes: timing does not depend on their values.
+
+@dataclass(frozen=True)
+class ModelConfig:
+    layers: int = 28
+    hidden: int = 1024
+    heads: int = 16
+    kv_heads: int = 8
+    head_dim: int = 128
+    intermediate: int = 3072
+    vocab: int = 151936
+    rope_theta: float = 1.0e6
+    eps: float = 1.0e-6
+
+
+QWEN3_06B = ModelConfig()
+
+_WEIGHT_SHAPES = {
+    "in_norm": lambda c: (c.hidden,),
+    "wq": lambda c: (c.hidden, c.heads * c.head_dim),
+    "wk": lambda c: (c.hidden, c.kv_heads * c.head_dim),
+    "wv": lambda c: (c.hidden, c.kv_heads * c.head_dim),
+    "q_norm": lambda c: (c.head_dim,),
+    "k_norm": lambda c: (c.head_dim,),
+    "wo": lambda c: (c.heads * c.head_dim, c.hidden),
+    "post_norm": lambda c: (c.hidden,),
+    "wg": lambda c: (c.hidden, c.intermediate),
+    "wu": lambda c: (c.hidden, c.intermediate),
+    "wd": lambda c: (c.intermediate, c.hidden),
+}
+
+
+def make_model_weights(cfg, seed, device="cpu"):
+    """Seeded random weights (bf16): "embed" [vocab, hidden] (tied output
+    head), "final_norm" [hidden], and per layer l the entries "l.<name>" of
+    _WEIGHT_SHAPES, projections stored [in, out] (x @ W).  Projection entries
+    are N(0, 1/in), norm gains 1 + N(0, 0.1^2), embeddings N(0, 1).  Drawn on
+    the host with PCG64 for device "cpu", else with a seeded torch generator
+    on the device (the full-size stack holds 0.6 G parameters)."""
+    out = {}
+    if device == "cpu":
+        rng = np.random.Generator(np.random.PCG64([seed, 4]))
+        draw = lambda shape: torch.from_numpy(rng.standard_normal(shape, dtype=np.float32))
+    else:
+        g = torch.Generator(device=device)
+        g.manual_seed(seed)
+        draw = lambda shape: torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+
+    def put(name, shape):
+        x = draw(shape)
+        if name.endswith("norm"):
+            x = 1.0 + 0.1 * x
+        elif name != "embed":
+            x = x / float(np.sqrt(shape[0]))
+        out[name] = x.to(torch.bfloat16)
+
+    put("embed", (cfg.vocab, cfg.hidden))
+    for l in range(cfg.layers):
+        for name, shape in _WEIGHT_SHAPES.items():
+            put(f"{l}.{name}", shape(cfg))
+    put("final_norm", (cfg.hidden,))
+    return out
+
+
+def make_tokens(cfg, n, seed):
+    """n token ids (int64 numpy), uniform over the vocabulary."""
+    rng = np.random.Generator(np.random.PCG64([seed, 5]))
+    return rng.integers(0, cfg.vocab, size=n, dtype=np.int64)

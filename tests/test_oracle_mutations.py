@@ -287,3 +287,43 @@ DECODE_PINS = [
 def test_decode_mutations_are_caught(monkeypatch, name, bad):
     monkeypatch.setattr(orc, name, bad)
     assert run_pins(DECODE_PINS)
+
+
+# ---------------------------------------------------------------------------
+# Whole-model prefill oracle
+# ---------------------------------------------------------------------------
+
+import test_oracle_model as TM
+from oracle import model_oracle as mo
+
+_rope = mo.rope
+_rms = mo.rms_norm
+
+
+def rope_sign_flip(x, theta):
+    n, _, d = x.shape
+    half = d // 2
+    inv = theta ** (-np.arange(0, d, 2, dtype=np.float64) / d)
+    ang = np.arange(n, dtype=np.float64)[:, None] * inv[None, :]
+    cos = np.concatenate([np.cos(ang), np.cos(ang)], axis=-1)[:, None, :]
+    sin = np.concatenate([np.sin(ang), np.sin(ang)], axis=-1)[:, None, :]
+    rotated = np.concatenate([x[..., half:], -x[..., :half]], axis=-1)     # wrong sign
+    return x * cos + rotated * sin
+
+
+def rms_without_eps_gain(x, w, eps):
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)       # gain dropped
+
+
+def relu_not_silu(x):
+    return np.maximum(x, 0.0)
+
+
+MODEL_PINS = [(TM.test_dense_stack_matches_transformers_qwen3, (37,))]
+
+
+@pytest.mark.parametrize("name,bad", [("rope", rope_sign_flip), ("rms_norm", rms_without_eps_gain),
+                                      ("silu", relu_not_silu)])
+def test_model_mutations_are_caught(monkeypatch, name, bad):
+    monkeypatch.setattr(mo, name, bad)
+    assert run_pins(MODEL_PINS)
