@@ -36,6 +36,10 @@ The last line of stdout is one JSON record:
              (host launch included); the dense decode through the same
              kernels next to it; achieved HBM GB/s on the algorithmic bytes
              (the K/V rows each token reads, its query and output)
+  ttft       whole-model prefill of the Qwen3-0.6B geometry with random
+             weights (§4.3, §5.3): warm time to first token at 8K / 16K / 32K
+             with every attention layer dense, the middle eight on the BF1
+             route, and all 28 on the BF1 route (timing only)
   cpu_baseline  the fp64 CPU oracle on a bounded sample of the workload
 
 --sweep additionally times n = 1K..64K for block widths 64 and 128 with the
@@ -74,6 +78,7 @@ def parse():
     ap.add_argument("--no-backward", action="store_true")
     ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-ttft", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time bound of the CPU oracle sample")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
@@ -301,6 +306,38 @@ def decode_point(torch, bf1, synth, w, reps):
     return rec
 
 
+def ttft_point(torch, synth, reps=5, warmup=2):
+    """Warm time to first token of the decoder stack, per context and
+    attention configuration (median of `reps` timed prefills)."""
+    from paper_2608_20427_amd.prefill_model import PrefillStack, middle_layers
+    cfg = synth.QWEN3_06B
+    st = PrefillStack(cfg, synth.make_model_weights(cfg, 6000, device="cuda"))
+    conds = {"dense": set(), "bf1_middle8": middle_layers(cfg, 8), "bf1_all": set(range(cfg.layers))}
+    out = {"model": "Qwen3-0.6B geometry, random weights", "bf1_middle8_layers": sorted(conds["bf1_middle8"]),
+           "contexts": {}}
+    for n in (8192, 16384, 32768):
+        ids = torch.from_numpy(synth.make_tokens(cfg, n, 6001)).cuda()
+        rec = {}
+        for name, sel in conds.items():
+            for _ in range(warmup):
+                st.last_logits(ids, sel)
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(reps):
+                t0 = time.perf_counter()
+                st.last_logits(ids, sel)
+                torch.cuda.synchronize()
+                ts.append((time.perf_counter() - t0) * 1e3)
+            rec[name + "_ms"] = statistics.median(ts)
+        rec["speedup_middle8"] = rec["dense_ms"] / rec["bf1_middle8_ms"]
+        rec["speedup_all"] = rec["dense_ms"] / rec["bf1_all_ms"]
+        out["contexts"][str(n)] = rec
+        del ids
+    del st
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -436,6 +473,13 @@ def main():
                 f"{d['bf1']['step_us_eager']:.1f} us eager ({d['bf1']['achieved_GBs']:.0f} GB/s), plan "
                 f"{d['bf1']['plan_us_graph']:.1f} us; dense step {d['dense']['step_us_graph']:.1f} us "
                 f"({d['dense']['achieved_GBs']:.0f} GB/s); speedup {d['speedup_vs_dense_graph']:.2f}x")
+
+    if not args.no_ttft:
+        tt = ttft_point(torch, synth)
+        rec["ttft"] = tt
+        for n, r in tt["contexts"].items():
+            log(f"ttft n={n}: dense {r['dense_ms']:.1f} ms, middle 8 BF1 {r['bf1_middle8_ms']:.1f} ms "
+                f"({r['speedup_middle8']:.2f}x), all BF1 {r['bf1_all_ms']:.1f} ms ({r['speedup_all']:.2f}x)")
 
     if args.sweep:
         os.makedirs(os.path.dirname(args.sweep_out), exist_ok=True)
