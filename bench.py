@@ -18,7 +18,10 @@ The last line of stdout is one JSON record:
              published dense bf16 MFMA peak of MI355X (2.5 PFLOP/s)
   dense      the in-house dense causal kernel timed with the paper's
              protocol (5 warmups, 30 reps, two opposite orders, median of the
-             two order medians, §4.3) next to BF1 timed the same way
+             two order medians, §4.3) next to BF1 timed the same way; PyTorch's
+             own scaled_dot_product_attention (the "native SDPA" the paper
+             compares against; flash backend only, K/V heads expanded to the
+             query heads) timed beside them
   backward   the backward (dQ, dK, dV) of the same layer, timed with the
              same two-order protocol next to the forward: one bf1_attn_bwd
              call (Delta, dQ, dK/dV and the partial-sum reduce) per rep,
@@ -164,6 +167,27 @@ def cpu_baseline(w, max_seconds):
                       f"workload {w.name}; fp64 NumPy gathered oracle, BLAS threads = host cores"}
 
 
+def sdpa_fn(torch, q, k, v):
+    """PyTorch's scaled_dot_product_attention (causal) restricted to its flash
+    backend, with K/V expanded to the query heads; None where that backend is
+    not available (its fallback paths are never used)."""
+    from torch.nn.attention import sdpa_kernel, SDPBackend
+    G = q.shape[1] // k.shape[1]
+    ke = k.repeat_interleave(G, dim=1).contiguous()
+    ve = v.repeat_interleave(G, dim=1).contiguous()
+
+    def f():
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            return torch.nn.functional.scaled_dot_product_attention(q, ke, ve, is_causal=True)
+    try:
+        f()
+        torch.cuda.synchronize()
+    except RuntimeError as e:
+        log(f"SDPA flash backend unavailable: {str(e)[:120]}")
+        return None
+    return f
+
+
 def run_point(torch, bf1, w, q, k, v, warmup, reps, with_dense=True):
     """Two-order timing of BF1 and dense on one workload."""
     o = torch.empty_like(q)
@@ -191,6 +215,12 @@ def run_point(torch, bf1, w, q, k, v, warmup, reps, with_dense=True):
                     "dense_pct_peak": 100 * dense_flops / sd["ms"] / 1e9 / PEAK_BF16_TFLOPS,
                     "speedup_vs_dense": sd["ms"] / sb["ms"],
                     "pair_reduction": dense_flops / flops})
+        f_sdpa = sdpa_fn(torch, q, k, v)
+        if f_sdpa is not None:
+            _, ss = two_order(torch, f_bf1, f_sdpa, warmup, reps)
+            rec.update({"sdpa_ms": ss["ms"], "sdpa_tflops": dense_flops / ss["ms"] / 1e9,
+                        "speedup_vs_sdpa": ss["ms"] / sb["ms"]})
+            del f_sdpa
     return rec
 
 
@@ -312,25 +342,44 @@ def ttft_point(torch, synth, reps=5, warmup=2):
     from paper_2608_20427_amd.prefill_model import PrefillStack, middle_layers
     cfg = synth.QWEN3_06B
     st = PrefillStack(cfg, synth.make_model_weights(cfg, 6000, device="cuda"))
-    conds = {"dense": set(), "bf1_middle8": middle_layers(cfg, 8), "bf1_all": set(range(cfg.layers))}
+    conds = {"dense": set(), "bf1_middle8": middle_layers(cfg, 8), "bf1_all": set(range(cfg.layers)),
+             "sdpa_dense": set(), "sdpa_bf1_middle8": middle_layers(cfg, 8)}
+    from torch.nn.attention import sdpa_kernel, SDPBackend
+
+    def sdpa(Q, K, V):
+        G = Q.shape[1] // K.shape[1]
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            return torch.nn.functional.scaled_dot_product_attention(
+                Q, K.repeat_interleave(G, dim=1), V.repeat_interleave(G, dim=1), is_causal=True)
+    probe = torch.zeros((1, 2, 64, 128), dtype=torch.bfloat16, device="cuda")
+    try:
+        sdpa(probe, probe[:, :1].contiguous(), probe[:, :1].contiguous())
+        torch.cuda.synchronize()
+    except RuntimeError:
+        conds.pop("sdpa_dense")
+        conds.pop("sdpa_bf1_middle8")
     out = {"model": "Qwen3-0.6B geometry, random weights", "bf1_middle8_layers": sorted(conds["bf1_middle8"]),
            "contexts": {}}
     for n in (8192, 16384, 32768):
         ids = torch.from_numpy(synth.make_tokens(cfg, n, 6001)).cuda()
         rec = {}
         for name, sel in conds.items():
+            dfn = sdpa if name.startswith("sdpa") else None
             for _ in range(warmup):
-                st.last_logits(ids, sel)
+                st.last_logits(ids, sel, dfn)
             torch.cuda.synchronize()
             ts = []
             for _ in range(reps):
                 t0 = time.perf_counter()
-                st.last_logits(ids, sel)
+                st.last_logits(ids, sel, dfn)
                 torch.cuda.synchronize()
                 ts.append((time.perf_counter() - t0) * 1e3)
             rec[name + "_ms"] = statistics.median(ts)
         rec["speedup_middle8"] = rec["dense_ms"] / rec["bf1_middle8_ms"]
         rec["speedup_all"] = rec["dense_ms"] / rec["bf1_all_ms"]
+        if "sdpa_dense_ms" in rec:
+            rec["speedup_middle8_vs_sdpa_dense"] = rec["sdpa_dense_ms"] / rec["sdpa_bf1_middle8_ms"]
+            rec["speedup_all_vs_sdpa_dense"] = rec["sdpa_dense_ms"] / rec["bf1_all_ms"]
         out["contexts"][str(n)] = rec
         del ids
     del st
@@ -449,7 +498,8 @@ def main():
         point = run_point(torch, bf1, w, q, k, v, args.warmup, args.reps)
         rec["paper_protocol"] = point
         log(f"two-order protocol: bf1 {point['bf1_ms']:.4f} ms, dense {point.get('dense_ms', 0):.4f} ms,"
-            f" speedup {point.get('speedup_vs_dense', 0):.2f}x")
+            f" speedup {point.get('speedup_vs_dense', 0):.2f}x; PyTorch SDPA {point.get('sdpa_ms', 0):.4f} ms,"
+            f" speedup {point.get('speedup_vs_sdpa', 0):.2f}x")
 
     if not args.no_backward:
         bp = backward_point(torch, bf1, synth, w, q, k, v, args.warmup, args.reps)
@@ -479,7 +529,10 @@ def main():
         rec["ttft"] = tt
         for n, r in tt["contexts"].items():
             log(f"ttft n={n}: dense {r['dense_ms']:.1f} ms, middle 8 BF1 {r['bf1_middle8_ms']:.1f} ms "
-                f"({r['speedup_middle8']:.2f}x), all BF1 {r['bf1_all_ms']:.1f} ms ({r['speedup_all']:.2f}x)")
+                f"({r['speedup_middle8']:.2f}x), all BF1 {r['bf1_all_ms']:.1f} ms ({r['speedup_all']:.2f}x); "
+                f"with PyTorch SDPA as the dense path: {r.get('sdpa_dense_ms', 0):.1f} ms -> "
+                f"{r.get('sdpa_bf1_middle8_ms', 0):.1f} ms ({r.get('speedup_middle8_vs_sdpa_dense', 0):.2f}x), "
+                f"all BF1 {r.get('speedup_all_vs_sdpa_dense', 0):.2f}x")
 
     if args.sweep:
         os.makedirs(os.path.dirname(args.sweep_out), exist_ok=True)
@@ -492,7 +545,8 @@ def main():
                     f.flush()
                     log(f"sweep n={sw.n} b={b}: bf1 {r['bf1_ms']:.4f} ms ({r['bf1_tflops']:.1f} TF/s,"
                         f" {r['bf1_pct_peak']:.1f}%), dense {r['dense_ms']:.4f} ms"
-                        f" ({r['dense_tflops']:.1f} TF/s), speedup {r['speedup_vs_dense']:.2f}x")
+                        f" ({r['dense_tflops']:.1f} TF/s), speedup {r['speedup_vs_dense']:.2f}x,"
+                        f" SDPA {r.get('sdpa_ms', 0):.4f} ms, speedup {r.get('speedup_vs_sdpa', 0):.2f}x")
                     del sq, sk, sv
 
     if not args.no_cpu_baseline:

@@ -58,9 +58,11 @@ class PrefillStack:
         rot = torch.cat([-xf[..., half:], xf[..., :half]], dim=-1)
         return (xf * cos + rot * sin).to(torch.bfloat16)
 
-    def last_logits(self, ids, bf1_layers):
+    def last_logits(self, ids, bf1_layers, dense_attention=None):
         """Logits (float32, [vocab]) of the last position after the prefill of
-        token ids (int64 device tensor [n])."""
+        token ids (int64 device tensor [n]).  dense_attention, if given,
+        replaces the in-house dense kernel for the non-BF1 layers: a callable
+        (Q, K, V) -> O on [1, heads, n, d] bf16 tensors (a comparator)."""
         cfg, w = self.cfg, self.w
         n = ids.shape[0]
         H, Hkv, d = cfg.heads, cfg.kv_heads, cfg.head_dim
@@ -78,6 +80,8 @@ class PrefillStack:
             V = v.transpose(0, 1).contiguous().unsqueeze(0)
             if l in bf1_layers:
                 O, _ = attn_fwd(Q, K, V, self.B, self.L, want_lse=False)
+            elif dense_attention is not None:
+                O = dense_attention(Q, K, V)
             else:
                 O, _ = dense_causal_fwd(Q, K, V, want_lse=False)
             h = h + O[0].transpose(0, 1).reshape(n, H * d) @ w[p + "wo"]
