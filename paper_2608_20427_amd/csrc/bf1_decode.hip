@@ -143,156 +143,104 @@ __device__ __forceinline__ bool step_view(const int32_t* __restrict__ seq_lens, 
 }
 
 template <int D, int G>
-__device__ __forceinline__ void write_nan(__bf16* O, float* LSE, int b, int Hq, int h, int tid) {
-    for (int x = tid; x < G * D; x += DEC_THREADS)
+__device__ __forceinline__ void write_nan(__bf16* O, float* LSE, int b, int Hq, int h, int tid, int nthreads) {
+    for (int x = tid; x < G * D; x += nthreads)
         O[((int64_t)b * Hq + h * G + x / D) * D + x % D] = (__bf16)__builtin_nanf("");
     if (LSE != nullptr && tid < G) LSE[(int64_t)b * Hq + h * G + tid] = __builtin_nanf("");
 }
 
-template <int D, int G, int PW>
-__global__ __launch_bounds__(DEC_THREADS) void decode_kernel(
-    const __bf16* __restrict__ Q, const __bf16* __restrict__ Kp, const __bf16* __restrict__ Vp,
-    const int32_t* __restrict__ seq_lens, int32_t num_pages, const int32_t* __restrict__ plan,
-    int32_t stride, int32_t cap, __bf16* __restrict__ O, float* __restrict__ LSE,
-    float* __restrict__ ws, int32_t Hkv, int32_t nsplit, int32_t ppw, float c_log2) {
-    constexpr int LPR = D / 8;            // lanes per key row (16 bytes each)
-    constexpr int RPI = 64 / LPR;         // key rows per wave-wide load
-    constexpr int KPW = PW / DEC_WAVES;   // keys of a page per wave
-    constexpr int NI = KPW / RPI;         // loads per page per wave (for K, and for V)
-    constexpr int REC = G * (D + 2);      // floats per partial record
+// A unit of decode work for one wave: a quarter of a page (KPW consecutive
+// keys), read as NI wave-wide loads of K rows and of V rows; lane `lane` holds
+// the 16-byte chunk cch of key row rg of every load.
+template <int D, int PW>
+struct Unit {
+    static constexpr int LPR = D / 8;    // lanes per key row (16 bytes each)
+    static constexpr int RPI = 64 / LPR;  // key rows per wave-wide load
+    static constexpr int KPW = PW / 4;    // keys per unit (a quarter page)
+    static constexpr int NI = KPW / RPI;  // loads per unit (for K, and for V)
     static_assert(NI >= 1 && KPW % RPI == 0, "page width and head_dim mismatch");
+};
 
-    __shared__ float red[DEC_WAVES][G][D + 2];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int rg = lane / LPR;
-    const int cch = lane % LPR;
-    const int s = blockIdx.x % nsplit;
-    const int bh = blockIdx.x / nsplit;
-    const int h = bh % Hkv;
-    const int b = bh / Hkv;
-    const int Hq = Hkv * G;
-    const int32_t* row = plan + (int64_t)b * stride;
-
-    StepView sv;
-    if (!step_view(seq_lens, row, cap, PW, b, &sv)) {
-        // stale or unplannable: the outputs of this (sequence, kv-head) are NaN
-        if (s == 0) write_nan<D, G>(O, LSE, b, Hq, h, tid);
-        return;
+template <int D, int PW>
+__device__ __forceinline__ void load_unit(const __bf16* __restrict__ Kp, const __bf16* __restrict__ Vp,
+                                          int64_t page_base, int quarter, int rg, int cch, u32x4* kr,
+                                          u32x4* vr) {
+    using U = Unit<D, PW>;
+#pragma unroll
+    for (int i = 0; i < U::NI; ++i) {
+        const int key = quarter * U::KPW + i * U::RPI + rg;
+        kr[i] = *reinterpret_cast<const u32x4*>(Kp + page_base + (int64_t)key * D + cch * 8);
     }
-    const int c = sv.c;
-    const int npages = c + 1;
-    const int nsb = (npages + ppw - 1) / ppw;
-    if (s >= nsb) return;
-    const int p0 = s * ppw;
-    const int p1 = min(npages, p0 + ppw);
-
-    float qv[G][8];
 #pragma unroll
-    for (int e = 0; e < G; ++e) {
-        const u32x4 w = *reinterpret_cast<const u32x4*>(Q + ((int64_t)b * Hq + h * G + e) * D + cch * 8);
-        bf16x8_to_float(w, qv[e]);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) qv[e][k] *= c_log2;
+    for (int i = 0; i < U::NI; ++i) {
+        const int key = quarter * U::KPW + i * U::RPI + rg;
+        vr[i] = *reinterpret_cast<const u32x4*>(Vp + page_base + (int64_t)key * D + cch * 8);
     }
+}
 
-    float m_run[G], l_run[G], o_acc[G][8];
+// Online softmax over one unit: the G scores of each key row (cross-lane sum
+// over the LPR lanes of the row), masked past nvalid keys of the page (their
+// V chunks zeroed), folded into the wave's running max / sum / row.
+template <int D, int G, int PW>
+__device__ __forceinline__ void consume_unit(const u32x4* kr, const u32x4* vr, int quarter, int rg, int nvalid,
+                                             const float (&qv)[G][8], float (&m_run)[G], float (&l_run)[G],
+                                             float (&o_acc)[G][8]) {
+    using U = Unit<D, PW>;
+    constexpr int NI = U::NI;
+    float sc[G][NI];
 #pragma unroll
-    for (int e = 0; e < G; ++e) {
-        m_run[e] = -INFINITY;
-        l_run[e] = 0.f;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) o_acc[e][k] = 0.f;
-    }
-
-    // K and V rows of page p of the split's list go to kr / vr; with PREFETCH
-    // the next page's loads are issued before the current page is consumed
-    // (where registers allow), so a wave keeps two pages of loads in flight.
-    constexpr bool PREFETCH = G * NI <= 16;
-    auto load_page = [&](int p, u32x4* kr, u32x4* vr) {
-        // pages written by the planner are in range; the clamp only keeps a
-        // foreign plan row from addressing memory outside the cache
-        const int32_t page = min(max(row[2 + p], 0), num_pages - 1);
-        const int64_t base = ((int64_t)page * Hkv + h) * PW * D;
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            const int key = wave * KPW + i * RPI + rg;
-            kr[i] = *reinterpret_cast<const u32x4*>(Kp + base + (int64_t)key * D + cch * 8);
-        }
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            const int key = wave * KPW + i * RPI + rg;
-            vr[i] = *reinterpret_cast<const u32x4*>(Vp + base + (int64_t)key * D + cch * 8);
-        }
-    };
-    u32x4 kr[NI], vr[NI];
-    if constexpr (PREFETCH) load_page(p0, kr, vr);
-    for (int p = p0; p < p1; ++p) {
-        const int nvalid = p < c ? PW : (int)(sv.t - sv.j * PW + 1);
-        u32x4 kn[NI], vn[NI];
-        if constexpr (PREFETCH) {
-            if (p + 1 < p1) load_page(p + 1, kn, vn);
-        } else {
-            load_page(p, kr, vr);
-        }
-        float sc[G][NI];
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            float kf[8];
-            bf16x8_to_float(kr[i], kf);
-#pragma unroll
-            for (int e = 0; e < G; ++e) {
-                float acc = 0.f;
-#pragma unroll
-                for (int k = 0; k < 8; ++k) acc = fmaf(qv[e][k], kf[k], acc);
-                sc[e][i] = acc;
-            }
-        }
-        // sum over the LPR lanes of a row
-#pragma unroll
-        for (int x = 1; x < LPR; x <<= 1)
-#pragma unroll
-            for (int e = 0; e < G; ++e)
-#pragma unroll
-                for (int i = 0; i < NI; ++i) sc[e][i] += __shfl_xor(sc[e][i], x);
-        bool valid[NI];
-#pragma unroll
-        for (int i = 0; i < NI; ++i) valid[i] = wave * KPW + i * RPI + rg < nvalid;
+    for (int i = 0; i < NI; ++i) {
+        float kf[8];
+        bf16x8_to_float(kr[i], kf);
 #pragma unroll
         for (int e = 0; e < G; ++e) {
-            float mx = -INFINITY;
+            float acc = 0.f;
 #pragma unroll
-            for (int i = 0; i < NI; ++i) mx = fmaxf(mx, valid[i] ? sc[e][i] : -INFINITY);
-#pragma unroll
-            for (int x = LPR; x < 64; x <<= 1) mx = fmaxf(mx, __shfl_xor(mx, x));
-            const float m_new = fmaxf(m_run[e], mx);
-            if (m_new == -INFINITY) continue;  // no visible key for this wave so far
-            const float alpha = exp2f(m_run[e] - m_new);
-            m_run[e] = m_new;
-            l_run[e] *= alpha;
-#pragma unroll
-            for (int k = 0; k < 8; ++k) o_acc[e][k] *= alpha;
-#pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                const float pr = valid[i] ? exp2f(sc[e][i] - m_new) : 0.f;
-                l_run[e] += pr;
-                float vf[8];
-                bf16x8_to_float(valid[i] ? vr[i] : u32x4{0u, 0u, 0u, 0u}, vf);
-#pragma unroll
-                for (int k = 0; k < 8; ++k) o_acc[e][k] = fmaf(pr, vf[k], o_acc[e][k]);
-            }
-        }
-        if constexpr (PREFETCH) {
-#pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                kr[i] = kn[i];
-                vr[i] = vn[i];
-            }
+            for (int k = 0; k < 8; ++k) acc = fmaf(qv[e][k], kf[k], acc);
+            sc[e][i] = acc;
         }
     }
-    // wave totals: sum over the RPI rows of each load
+#pragma unroll
+    for (int x = 1; x < U::LPR; x <<= 1)
+#pragma unroll
+        for (int e = 0; e < G; ++e)
+#pragma unroll
+            for (int i = 0; i < NI; ++i) sc[e][i] += __shfl_xor(sc[e][i], x);
+    bool valid[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) valid[i] = quarter * U::KPW + i * U::RPI + rg < nvalid;
+#pragma unroll
+    for (int e = 0; e < G; ++e) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) mx = fmaxf(mx, valid[i] ? sc[e][i] : -INFINITY);
+#pragma unroll
+        for (int x = U::LPR; x < 64; x <<= 1) mx = fmaxf(mx, __shfl_xor(mx, x));
+        const float m_new = fmaxf(m_run[e], mx);
+        if (m_new == -INFINITY) continue;  // no visible key for this wave so far
+        const float alpha = exp2f(m_run[e] - m_new);
+        m_run[e] = m_new;
+        l_run[e] *= alpha;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) o_acc[e][k] *= alpha;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const float pr = valid[i] ? exp2f(sc[e][i] - m_new) : 0.f;
+            l_run[e] += pr;
+            float vf[8];
+            bf16x8_to_float(valid[i] ? vr[i] : u32x4{0u, 0u, 0u, 0u}, vf);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) o_acc[e][k] = fmaf(pr, vf[k], o_acc[e][k]);
+        }
+    }
+}
+
+// The wave's totals (sums over the RPI key rows of each load) into LDS slot
+// red[wave]: max, sum, unnormalised row.
+template <int D, int G>
+__device__ __forceinline__ void wave_totals_to_lds(float (&red)[G][D + 2], int lane, int rg, int cch,
+                                                   float (&m_run)[G], float (&l_run)[G], float (&o_acc)[G][8]) {
+    constexpr int LPR = D / 8;
 #pragma unroll
     for (int x = LPR; x < 64; x <<= 1)
 #pragma unroll
@@ -305,15 +253,111 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_kernel(
 #pragma unroll
         for (int e = 0; e < G; ++e)
 #pragma unroll
-            for (int k = 0; k < 8; ++k) red[wave][e][2 + cch * 8 + k] = o_acc[e][k];
+            for (int k = 0; k < 8; ++k) red[e][2 + cch * 8 + k] = o_acc[e][k];
     }
     if (lane == 0) {
 #pragma unroll
         for (int e = 0; e < G; ++e) {
-            red[wave][e][0] = m_run[e];
-            red[wave][e][1] = l_run[e];
+            red[e][0] = m_run[e];
+            red[e][1] = l_run[e];
         }
     }
+}
+
+template <int D, int G>
+__device__ __forceinline__ void load_query(const __bf16* __restrict__ Q, int b, int Hq, int h, int cch,
+                                           float c_log2, float (&qv)[G][8]) {
+#pragma unroll
+    for (int e = 0; e < G; ++e) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(Q + ((int64_t)b * Hq + h * G + e) * D + cch * 8);
+        bf16x8_to_float(w, qv[e]);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) qv[e][k] *= c_log2;
+    }
+}
+
+template <int G>
+__device__ __forceinline__ void init_running(float (&m_run)[G], float (&l_run)[G], float (&o_acc)[G][8]) {
+#pragma unroll
+    for (int e = 0; e < G; ++e) {
+        m_run[e] = -INFINITY;
+        l_run[e] = 0.f;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) o_acc[e][k] = 0.f;
+    }
+}
+
+template <int D, int G, int PW>
+__global__ __launch_bounds__(DEC_THREADS) void decode_kernel(
+    const __bf16* __restrict__ Q, const __bf16* __restrict__ Kp, const __bf16* __restrict__ Vp,
+    const int32_t* __restrict__ seq_lens, int32_t num_pages, const int32_t* __restrict__ plan,
+    int32_t stride, int32_t cap, __bf16* __restrict__ O, float* __restrict__ LSE,
+    float* __restrict__ ws, int32_t Hkv, int32_t nsplit, int32_t ppw, float c_log2) {
+    using U = Unit<D, PW>;
+    constexpr int NI = U::NI;
+    constexpr int REC = G * (D + 2);      // floats per partial record
+
+    __shared__ float red[DEC_WAVES][G][D + 2];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int rg = lane / U::LPR;
+    const int cch = lane % U::LPR;
+    const int s = blockIdx.x % nsplit;
+    const int bh = blockIdx.x / nsplit;
+    const int h = bh % Hkv;
+    const int b = bh / Hkv;
+    const int Hq = Hkv * G;
+    const int32_t* row = plan + (int64_t)b * stride;
+
+    StepView sv;
+    if (!step_view(seq_lens, row, cap, PW, b, &sv)) {
+        // stale or unplannable: the outputs of this (sequence, kv-head) are NaN
+        if (s == 0) write_nan<D, G>(O, LSE, b, Hq, h, tid, DEC_THREADS);
+        return;
+    }
+    const int c = sv.c;
+    const int npages = c + 1;
+    const int nsb = (npages + ppw - 1) / ppw;
+    if (s >= nsb) return;
+    const int p0 = s * ppw;
+    const int p1 = min(npages, p0 + ppw);
+
+    float qv[G][8];
+    load_query<D, G>(Q, b, Hq, h, cch, c_log2, qv);
+    float m_run[G], l_run[G], o_acc[G][8];
+    init_running<G>(m_run, l_run, o_acc);
+
+    // Wave w takes quarter w of every page of the split; with PREFETCH the
+    // next page's loads are issued before the current page is consumed (where
+    // registers allow), so a wave keeps two pages of loads in flight.  Pages
+    // written by the planner are in range; the clamp only keeps a foreign plan
+    // row from addressing memory outside the cache.
+    constexpr bool PREFETCH = G * NI <= 16;
+    auto page_base = [&](int p) {
+        return ((int64_t)min(max(row[2 + p], 0), num_pages - 1) * Hkv + h) * PW * D;
+    };
+    u32x4 kr[NI], vr[NI];
+    if constexpr (PREFETCH) load_unit<D, PW>(Kp, Vp, page_base(p0), wave, rg, cch, kr, vr);
+    for (int p = p0; p < p1; ++p) {
+        const int nvalid = p < c ? PW : (int)(sv.t - sv.j * PW + 1);
+        u32x4 kn[NI], vn[NI];
+        if constexpr (PREFETCH) {
+            if (p + 1 < p1) load_unit<D, PW>(Kp, Vp, page_base(p + 1), wave, rg, cch, kn, vn);
+        } else {
+            load_unit<D, PW>(Kp, Vp, page_base(p), wave, rg, cch, kr, vr);
+        }
+        consume_unit<D, G, PW>(kr, vr, wave, rg, nvalid, qv, m_run, l_run, o_acc);
+        if constexpr (PREFETCH) {
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                kr[i] = kn[i];
+                vr[i] = vn[i];
+            }
+        }
+    }
+    wave_totals_to_lds<D, G>(red[wave], lane, rg, cch, m_run, l_run, o_acc);
     __syncthreads();
 
     const bool single = nsb == 1;

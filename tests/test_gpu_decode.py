@@ -129,6 +129,27 @@ def test_decode_small_full_oracle(cfg):
     compare(o, l, o_ref, l_ref, str(cfg))
 
 
+# Larger batches: more (sequence, kv-head) pairs than pages per list, so
+# several pages share a split and the merge folds fewer records.
+SPLIT = [
+    # batch, Hq, Hkv, d, B, L, seq_lens: 320 / 288 (sequence, kv-head) pairs,
+    # so a split holds 3 / 2 pages of each list (about 1024 workgroups)
+    (40, 16, 8, 128, 64, 2, [1, 64, 65, 1000, 2048, 3001, 777, 130, 4096, 5] * 4),
+    (36, 16, 8, 64, 128, 1, [1, 128, 129, 900, 1500, 60, 3000, 2048, 255, 256, 257, 1024] * 3),
+]
+
+
+@pytest.mark.parametrize("cfg", SPLIT, ids=lambda c: "x".join(map(str, c[:6])))
+def test_decode_split_path_full_oracle(cfg):
+    batch, Hq, Hkv, d, B, L, lens = cfg
+    w = synth.DecodeWorkload("dec", batch, max(lens), Hq, Hkv, d, B, L, seed=700 + batch)
+    say(f"decode split path {cfg[:6]}")
+    (q, k, v, sl, _), dev = setup_case(w, np.array(lens, dtype=np.int32))
+    o, l, _ = run_decode(w, dev)
+    o_ref, l_ref = orc.attn_decode_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), sl, B, L)
+    compare(o, l, o_ref, l_ref, "split " + str(cfg[:6]))
+
+
 def test_decode_dense_plan_is_dense_causal():
     w = synth.DecodeWorkload("dec", 3, 2000, 4, 2, 128, 64, 2, seed=77)
     lens = np.array([2000, 65, 1], dtype=np.int32)
@@ -221,7 +242,7 @@ def test_decode_deterministic_and_plan_unchanged():
 # Full size (the timed configurations), oracle on sampled sequences
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name", ["decode_n32768_batch8", "decode_n65536_batch1"])
+@pytest.mark.parametrize("name", ["decode_n32768_batch8", "decode_n65536_batch1", "decode_n32768_batch32"])
 def test_decode_full_size_sampled(name):
     w = synth.DECODE_WORKLOADS[name]
     say(f"decode full size {name}")
