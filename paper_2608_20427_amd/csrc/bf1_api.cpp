@@ -65,17 +65,14 @@ int check_attn(const void* Q, const void* K, const void* V, void* O, float* LSE,
 
 // ---- decode ----------------------------------------------------------------
 // Earlier selected pages any token of a sequence of at most max_seq_len
-// tokens can need: max over j < NB of c(j) (every earlier block if dense).
+// tokens can need: the largest c(j) over j < NB, which is c(NB - 1) because
+// c never decreases (j <= L: c = j; beyond, the locals stay L, the dyadic
+// count only grows, and where block 0 stops being a separate entry (j a power
+// of two) the dyadic count has just grown by one), or NB - 1 if dense.
 bool decode_cap(int64_t max_seq_len, int64_t B, int64_t L, bool dense, int64_t* cap) {
     const int64_t NB = (max_seq_len + B - 1) / B;
     if (NB < 1 || NB >= 0x7fffffff) return false;
-    if (dense) {
-        *cap = NB - 1;
-        return true;
-    }
-    int64_t c = 0;
-    for (int64_t j = 0; j < NB; ++j) c = std::max(c, bf1::route_pred_count(j, L));
-    *cap = c;
+    *cap = dense ? NB - 1 : bf1::route_pred_count(NB - 1, L);
     return true;
 }
 
