@@ -194,3 +194,44 @@ def test_backward_chained_from_gpu_forward():
         err = np.abs(got.cpu().double().numpy() - r).max()
         say(f"  chained {name}: max err {err:.3e} (max |ref| {np.abs(r).max():.3e})")
         assert err <= 2e-2 * np.abs(r).max(), name
+
+
+def test_backward_peaked_rows_ragged_batch():
+    # The partial-block / batching workload's structure at a small size: batch
+    # 2, a ragged length, K scaled x3 on 5% of the positions (peaked softmax
+    # rows, where recomputing P from the LSE is most sensitive).
+    w = synth.Workload("bwd_peaked", 2, 1501, 4, 2, 128, 64, 2, seed=3, peak_frac=0.05, peak_mul=3.0)
+    say("backward peaked rows, batch 2, n = 1501")
+    (dq, dk, dv), ref, terms = run_case(w)
+    for name, got, r, t in zip(("dQ", "dK", "dV"), (dq, dk, dv), ref, terms):
+        check_bound(got, r, t, tag=f"peaked {name}")
+
+
+def test_backward_full_size_peaked_sampled():
+    # The full n = 30001, batch 2 peaked workload: sampled blocks of both
+    # batch elements, including the 49-token last block and key block 0.
+    w = synth.WORKLOADS["qwen_n30001_b2_peaked"]
+    say("backward n=30001 batch 2 peaked, sampled")
+    NB = orc.num_blocks(w.n, w.b)
+    q, k, v = synth.make_qkv(w)
+    do = synth.make_grad_out(w)
+    qf, kf, vf, dof = (synth.to_f64(t) for t in (q, k, v, do))
+    qb = [0, 2, 250, NB - 1]
+    kv = [3, 200, NB - 2, NB - 1]
+    rp_t, ci_t = orc.csr_transposed(w.n, w.b, w.L)
+    need = sorted(set(qb) | {int(j) for i in kv for j in ci_t[rp_t[i]:rp_t[i + 1]]})
+    o_ref, lse_ref = orc.attn_gathered_fp64(qf, kf, vf, w.b, w.L, blocks=need)
+    o_ref, lse_ref = np.nan_to_num(o_ref), np.nan_to_num(lse_ref)
+    o_bf = torch.from_numpy(o_ref).to(torch.bfloat16)
+    o_used = synth.to_f64(o_bf)
+    dq, dk, dv = bf1.attn_bwd(q.cuda(), k.cuda(), v.cuda(), o_bf.cuda(), do.cuda(),
+                              torch.from_numpy(lse_ref.astype(np.float32)).cuda(), w.b, w.L)
+    torch.cuda.synchronize()
+    ref = orc.attn_bwd_gathered_fp64(qf, kf, vf, dof, w.b, w.L, o=o_used, q_blocks=qb, kv_blocks=kv)
+    terms = list(zip(
+        orc.attn_bwd_abs_terms_fp64(qf, kf, vf, dof, w.b, w.L, o=o_used, q_blocks=qb, kv_blocks=kv),
+        orc.attn_bwd_abs_terms_fp64(qf, kf, vf, dof, w.b, w.L, o=o_used, q_blocks=qb, kv_blocks=kv,
+                                    kind="pdp")))
+    check_bound(dq, ref[0], terms[0], rows=_rows(qb, w.b, w.n), tag="30001 dQ")
+    check_bound(dk, ref[1], terms[1], rows=_rows(kv, w.b, w.n), tag="30001 dK")
+    check_bound(dv, ref[2], terms[2], rows=_rows(kv, w.b, w.n), tag="30001 dV")
