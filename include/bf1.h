@@ -140,16 +140,16 @@ int bf1_plan_transposed(int64_t n, int32_t B, int32_t L,
  *     P = exp(Q K^T / sqrt(d) - LSE),  D = rowsum(dO * O),  dS = P * (dO V^T - D),
  *     dQ = dS K / sqrt(d),  dK = dS^T Q / sqrt(d),  dV = P^T dO,
  * dK and dV summed over the q-heads of each GQA group.
- *   Q, O, dO : [batch, Hq, n, 128] bf16 (O and LSE as written by bf1_attn_fwd)
- *   K, V     : [batch, Hkv, n, 128] bf16
+ *   Q, O, dO : [batch, Hq, n, head_dim] bf16 (O and LSE as written by bf1_attn_fwd)
+ *   K, V     : [batch, Hkv, n, head_dim] bf16
  *   LSE      : [batch, Hq, n] fp32, natural log
- *   dQ       : [batch, Hq, n, 128] fp32 (caller-owned, overwritten)
- *   dK, dV   : [batch, Hkv, n, 128] fp32 (caller-owned, overwritten)
+ *   dQ       : [batch, Hq, n, head_dim] fp32 (caller-owned, overwritten)
+ *   dK, dV   : [batch, Hkv, n, head_dim] fp32 (caller-owned, overwritten)
  *   workspace: caller-owned device scratch of at least
  *              bf1_attn_bwd_workspace_size() bytes, 256-byte aligned; its
  *              contents on entry are irrelevant and are clobbered.
- * Supported: head_dim 128, B in {64, 128}, G = Hq/Hkv in {1, 2, 4, 8} with
- * G * B >= 128 (so G = 1 needs B = 128); others return BF1_ERR_UNSUPPORTED.
+ * Supported: head_dim in {64, 128}, B in {64, 128}, G = Hq/Hkv in {1, 2, 4, 8}
+ * with G * B >= 128 (so G = 1 needs B = 128); others return BF1_ERR_UNSUPPORTED.
  * Three kernels on `stream`: dQ (also writes D to the workspace), dK/dV
  * over the transposed route (cut into segments of at most 16 query blocks;
  * the segments of long lists -- block 0 -- leave partial sums in the

@@ -203,12 +203,12 @@ struct BwdPlan {
 };
 std::map<std::tuple<int, int64_t, int32_t, int32_t>, BwdPlan> g_bwd_plans;
 
-int bwd_workspace_bytes(int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t B, int32_t L,
-                        int64_t* bytes) {
+int bwd_workspace_bytes(int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t B,
+                        int32_t L, int64_t* bytes) {
     BwdLayout lay;
     if (!bwd_layout(n, B, L, &lay, false)) return BF1_ERR_INVALID_ARG;
     const int64_t delta = ((int64_t)batch * Hq * n * 4 + 255) / 256 * 256;
-    const int64_t part = (int64_t)batch * Hkv * lay.nslots * 2 * 64 * 128 * 4;
+    const int64_t part = (int64_t)batch * Hkv * lay.nslots * 2 * 64 * head_dim * 4;
     *bytes = delta + part;
     return BF1_OK;
 }
@@ -435,8 +435,8 @@ int bf1_attn_bwd_workspace_size(int32_t batch, int64_t n, int32_t Hq, int32_t Hk
     int st = check_attn(nullptr, nullptr, nullptr, nullptr, nullptr, 0, n, Hq, Hkv, head_dim);
     if (st != BF1_OK) return st;
     if (batch < 0 || L < 0) return BF1_ERR_INVALID_ARG;
-    if (head_dim != 128 || (B != 64 && B != 128) || (Hq / Hkv) * B < 128) return BF1_ERR_UNSUPPORTED;
-    return bwd_workspace_bytes(batch, n, Hq, Hkv, B, L, bytes);
+    if ((B != 64 && B != 128) || (Hq / Hkv) * B < 128) return BF1_ERR_UNSUPPORTED;
+    return bwd_workspace_bytes(batch, n, Hq, Hkv, head_dim, B, L, bytes);
 }
 
 int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, const void* dO,
@@ -446,14 +446,14 @@ int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, con
     int st = check_attn(Q, K, V, const_cast<void*>(O), nullptr, batch, n, Hq, Hkv, head_dim);
     if (st != BF1_OK) return st;
     if (L < 0 || workspace_bytes < 0) return BF1_ERR_INVALID_ARG;
-    if (head_dim != 128 || (B != 64 && B != 128) || (Hq / Hkv) * B < 128) return BF1_ERR_UNSUPPORTED;
+    if ((B != 64 && B != 128) || (Hq / Hkv) * B < 128) return BF1_ERR_UNSUPPORTED;
     if (batch == 0 || n == 0) return BF1_OK;
     if (!dO || !LSE || !dQ || !dK || !dV || !workspace) return BF1_ERR_INVALID_ARG;
     if (!aligned(dO, 16) || !aligned(dQ, 16) || !aligned(dK, 16) || !aligned(dV, 16) ||
         !aligned(LSE, 4) || !aligned(workspace, 256))
         return BF1_ERR_INVALID_ARG;
     int64_t need = 0;
-    st = bwd_workspace_bytes(batch, n, Hq, Hkv, B, L, &need);
+    st = bwd_workspace_bytes(batch, n, Hq, Hkv, head_dim, B, L, &need);
     if (st != BF1_OK) return st;
     if (workspace_bytes < need) return BF1_ERR_BUFFER_TOO_SMALL;
     hipStream_t s = (hipStream_t)stream;
@@ -468,7 +468,7 @@ int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, con
     float* part = (float*)((char*)workspace + delta_bytes);
     bf1::BwdArgs a{Q, K, V, O, dO, LSE, dQ, dK, dV, delta, part,
                    plan.row_ptr, plan.col_idx, plan.nnz, bp.users, bp.segs, bp.nseg,
-                   bp.reds, bp.nred, bp.nslots, batch, n, Hq, Hkv, B};
+                   bp.reds, bp.nred, bp.nslots, batch, n, Hq, Hkv, B, head_dim};
     return status_of(bf1::launch_backward(a, s));
 }
 

@@ -34,29 +34,42 @@
 namespace bf1 {
 namespace {
 
-constexpr int BD = 128;          // head_dim of the backward kernels
-constexpr int BRB = BD * 2;      // bytes per bf16 row
-constexpr int BTILE = KT * BRB;  // bytes per 64-row tile (16 KB)
-constexpr int BKS = BD / 16;     // MFMA k-steps along d
-constexpr int BDT = BD / 32;     // 32-wide d tiles
+// head_dim D of a backward instance: bytes per bf16 row, per 64-row tile,
+// MFMA k-steps along d, 32-wide d tiles, 16-byte chunks per row
+#define BWD_GEOMETRY(D)                                                     \
+    constexpr int BD = (D), BRB = 2 * (D), BTILE = KT * BRB, BKS = (D) / 16, \
+                  BDT = (D) / 32;                                           \
+    (void)BD; (void)BRB; (void)BTILE; (void)BKS; (void)BDT
 
-__device__ __forceinline__ int bswz(int row) { return 4 * (row & 3) + ((row >> 2) & 3); }
+// Physical chunk swizzle of row `row`: chunk c of the row sits at c ^ bswz.
+// Chosen (by simulating the 64 banks) so that both reads of a tile are
+// conflict-free: 16 lanes reading 16 bytes of 16 consecutive rows (the
+// row-wise operand), and 32 lanes of the transpose load reading 8 bytes each.
+template <int D>
+__device__ __forceinline__ int bswz(int row) {
+    if constexpr (D == 128) return 4 * (row & 3) + ((row >> 2) & 3);
+    else return (((row >> 1) & 1) << 2) | (((row >> 3) & 1) << 1) | ((row >> 2) & 1);
+}
 
 // Byte offset, inside a tile, of the 16 bytes lane `lane` moves in the direct
-// load of 1 KB segment `seg` (rows 4 seg .. 4 seg + 3, lane order = physical).
+// load of 1 KB segment `seg` (1024 / (2 D) rows, lane order = physical).
+template <int D>
 __device__ __forceinline__ uint32_t seg_off(int seg, int lane) {
-    const int row = seg * 4 + (lane >> 4), pc = lane & 15;
-    return (uint32_t)(row * BRB + ((pc ^ bswz(row)) << 4));
+    constexpr int CH = D / 8;
+    const int row = seg * (64 / CH) + lane / CH, pc = lane % CH;
+    return (uint32_t)(row * 2 * D + ((pc ^ bswz<D>(row)) << 4));
 }
 // Row-wise operand read: 16 bytes of `row`, logical chunk c.
-__device__ __forceinline__ int rw_off(int row, int c) { return row * BRB + ((c ^ bswz(row)) << 4); }
+template <int D>
+__device__ __forceinline__ int rw_off(int row, int c) { return row * 2 * D + ((c ^ bswz<D>(row)) << 4); }
 // Transpose-read base of lane `lane` for d-tile dt, second read of a pair h2
 // (rows +8); a 16-row group g adds 16 g rows (bswz is unchanged by it).
+template <int D>
 __device__ __forceinline__ int tr_off(int lane, int dt, int h2) {
     const int gq = lane >> 4, kk = lane & 15;
     const int row = 4 * (gq >> 1) + (kk >> 2) + 8 * h2;
     const int lb = 32 * (2 * dt + (gq & 1)) + 8 * (kk & 3);
-    return row * BRB + (((lb >> 4) ^ bswz(row)) << 4) + (lb & 15);
+    return row * 2 * D + (((lb >> 4) ^ bswz<D>(row)) << 4) + (lb & 15);
 }
 
 __device__ __forceinline__ float dot_bf16x8(u32x4 a, u32x4 b) {
@@ -77,13 +90,14 @@ __device__ __forceinline__ float dot_bf16x8(u32x4 a, u32x4 b) {
 // dQ^T += K^T dS^T (A operand: transpose reads of the K tile; B: dS^T packed
 // to bf16 from the lane's own registers).  Double-buffered K/V tiles, one
 // barrier per tile.
-template <int G, int BW, bool DENSE>
+template <int D, int G, int BW, bool DENSE>
 __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ O, const __bf16* __restrict__ dO, const float* __restrict__ LSE,
     float* __restrict__ dQ, float* __restrict__ Delta, const int32_t* __restrict__ row_ptr,
     const int32_t* __restrict__ col_idx, int64_t nnz, int32_t n, int32_t NB, int32_t batch_hkv,
     int32_t Hkv, float c_log2, float scale) {
+    BWD_GEOMETRY(D);
     constexpr int NW = 4, ROWS = 128;
     constexpr int NCHUNK = (G * BW) / ROWS;
     constexpr int NSUB = BW / KT;
@@ -183,8 +197,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
 #pragma unroll
         for (int it = 0; it < SPW; ++it) {
             const int seg = it * NW + wave;
-            load_lds_async<16>(k_rsrc, &kt_s[buf][seg * 64], seg_off(seg, lane), soff);
-            load_lds_async<16>(v_rsrc, &vt_s[buf][seg * 64], seg_off(seg, lane), soff);
+            load_lds_async<16>(k_rsrc, &kt_s[buf][seg * 64], seg_off<D>(seg, lane), soff);
+            load_lds_async<16>(v_rsrc, &vt_s[buf][seg * 64], seg_off<D>(seg, lane), soff);
         }
     };
 
@@ -213,7 +227,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
             for (int ks = 0; ks < BKS; ++ks) {
-                const int o = rw_off(32 * kt + col, 2 * ks + half);
+                const int o = rw_off<D>(32 * kt + col, 2 * ks + half);
                 const u32x4 ka = *reinterpret_cast<const u32x4*>(kb + o);
                 const u32x4 va = *reinterpret_cast<const u32x4*>(vb + o);
                 st[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -239,7 +253,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
         const uint32_t kl = lds_addr(kb);
 #pragma unroll
         for (int dt = 0; dt < BDT; ++dt) {
-            const uint32_t a0 = kl + tr_off(lane, dt, 0), a1 = kl + tr_off(lane, dt, 1);
+            const uint32_t a0 = kl + tr_off<D>(lane, dt, 0), a1 = kl + tr_off<D>(lane, dt, 1);
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const u32x2 lo = lds_read_tr16(a0 + 16 * t * BRB);
@@ -287,13 +301,14 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
 // A segment descriptor (int32 x 8): key block, sub-tile, first entry of its
 // query-block list in the transposed table, entry count, partial slot (-1:
 // write dK/dV directly).
-template <int G, int BW>
+template <int D, int G, int BW>
 __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ Delta,
     float* __restrict__ dK, float* __restrict__ dV, float* __restrict__ part,
     const int32_t* __restrict__ segs, const int32_t* __restrict__ users, int32_t nslots,
     int32_t n, int32_t batch_hkv, int32_t Hkv, float c_log2, float scale) {
+    BWD_GEOMETRY(D);
     constexpr int NW = 2;
     constexpr int NSUB = BW / KT;
     constexpr int SPW = (BTILE / 1024) / NW;  // Q (or dO) segments per wave per tile
@@ -356,8 +371,8 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
 #pragma unroll
         for (int it = 0; it < SPW; ++it) {
             const int seg = it * NW + wave;
-            load_lds_async<16>(qr, &q_s[buf][seg * 64], seg_off(seg, lane), soff);
-            load_lds_async<16>(orr, &o_s[buf][seg * 64], seg_off(seg, lane), soff);
+            load_lds_async<16>(qr, &q_s[buf][seg * 64], seg_off<D>(seg, lane), soff);
+            load_lds_async<16>(orr, &o_s[buf][seg * 64], seg_off<D>(seg, lane), soff);
         }
         // 64 rows of LSE (wave 0) or D (wave 1), 4 bytes per lane
         const float* src = (wave == 0 ? LSE : Delta) + qr0;
@@ -389,7 +404,7 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
             f32x16 s, dp;
 #pragma unroll
             for (int ks = 0; ks < BKS; ++ks) {
-                const int o = rw_off(32 * rh + col, 2 * ks + half);
+                const int o = rw_off<D>(32 * rh + col, 2 * ks + half);
                 const u32x4 qa = *reinterpret_cast<const u32x4*>(qb + o);
                 const u32x4 oa = *reinterpret_cast<const u32x4*>(ob + o);
                 s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, qa), kf[ks],
@@ -419,10 +434,10 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
 #pragma unroll
                 for (int m = 0; m < 2; ++m) {
                     const int go = 16 * (2 * rh + m) * BRB;
-                    const u32x2 olo = lds_read_tr16(ol + tr_off(lane, dt, 0) + go);
-                    const u32x2 ohi = lds_read_tr16(ol + tr_off(lane, dt, 1) + go);
-                    const u32x2 qlo = lds_read_tr16(ql + tr_off(lane, dt, 0) + go);
-                    const u32x2 qhi = lds_read_tr16(ql + tr_off(lane, dt, 1) + go);
+                    const u32x2 olo = lds_read_tr16(ol + tr_off<D>(lane, dt, 0) + go);
+                    const u32x2 ohi = lds_read_tr16(ol + tr_off<D>(lane, dt, 1) + go);
+                    const u32x2 qlo = lds_read_tr16(ql + tr_off<D>(lane, dt, 0) + go);
+                    const u32x2 qhi = lds_read_tr16(ql + tr_off<D>(lane, dt, 1) + go);
                     const u32x4 wo = {olo[0], olo[1], ohi[0], ohi[1]};
                     const u32x4 wq = {qlo[0], qlo[1], qhi[0], qhi[1]};
                     dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa[m], __builtin_bit_cast(bf16x8, wo),
@@ -469,10 +484,11 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
 // workgroup per (descriptor, batch x kv-head, 512-element chunk of the 64 x 128
 // tile); each thread sums two elements of dK and of dV over the slots.
 constexpr int RED_CHUNK = 512;
-template <int BW>
+template <int D, int BW>
 __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     float* __restrict__ dK, float* __restrict__ dV, const float* __restrict__ part,
     const int32_t* __restrict__ reds, int32_t nslots, int32_t n, int32_t batch_hkv) {
+    BWD_GEOMETRY(D);
     constexpr int NCH = KT * BD / RED_CHUNK;
     const int32_t x = blockIdx.x;
     const int ch = x % NCH;
@@ -498,8 +514,9 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     }
 }
 
-template <int G, int BW>
+template <int D, int G, int BW>
 hipError_t launch_bwd_g(const BwdArgs& a, hipStream_t stream) {
+    BWD_GEOMETRY(D);
     constexpr int NCHUNK = (G * BW) / 128;
     const int32_t NB = (int32_t)((a.n + BW - 1) / BW);
     const int32_t bhk = a.batch * a.Hkv;
@@ -508,14 +525,14 @@ hipError_t launch_bwd_g(const BwdArgs& a, hipStream_t stream) {
         return hipErrorInvalidValue;
     const float scale = 1.0f / sqrtf((float)BD);
     const float c_log2 = scale * LOG2E;
-    hipLaunchKernelGGL((bwd_dq_kernel<G, BW, false>), dim3((unsigned)items), dim3(256), 0, stream,
+    hipLaunchKernelGGL((bwd_dq_kernel<D, G, BW, false>), dim3((unsigned)items), dim3(256), 0, stream,
                        (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, (const __bf16*)a.O,
                        (const __bf16*)a.dO, a.LSE, a.dQ, a.delta, a.row_ptr, a.col_idx, a.nnz,
                        (int32_t)a.n, NB, bhk, a.Hkv, c_log2, scale);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.nseg > 0) {
-        hipLaunchKernelGGL((bwd_dkdv_kernel<G, BW>), dim3((unsigned)(a.nseg * bhk)), dim3(128), 0,
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, G, BW>), dim3((unsigned)(a.nseg * bhk)), dim3(128), 0,
                            stream, (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
                            (const __bf16*)a.dO, a.LSE, a.delta, a.dK, a.dV, a.part, a.segs,
                            a.users, a.nslots, (int32_t)a.n, bhk, a.Hkv, c_log2, scale);
@@ -525,30 +542,34 @@ hipError_t launch_bwd_g(const BwdArgs& a, hipStream_t stream) {
     if (a.nred > 0) {
         const int64_t grid = (int64_t)a.nred * bhk * (KT * BD / RED_CHUNK);
         if (grid > 0x7fffffff) return hipErrorInvalidValue;
-        hipLaunchKernelGGL((bwd_reduce_kernel<BW>), dim3((unsigned)grid), dim3(256), 0,
+        hipLaunchKernelGGL((bwd_reduce_kernel<D, BW>), dim3((unsigned)grid), dim3(256), 0,
                            stream, a.dK, a.dV, a.part, a.reds, a.nslots, (int32_t)a.n, bhk);
         e = hipGetLastError();
     }
     return e;
 }
 
-template <int BW>
+template <int D, int BW>
 hipError_t launch_bwd_b(const BwdArgs& a, hipStream_t s) {
     switch (a.Hq / a.Hkv) {
         case 1:
-            if constexpr (BW >= 128) return launch_bwd_g<1, BW>(a, s);
+            if constexpr (BW >= 128) return launch_bwd_g<D, 1, BW>(a, s);
             return hipErrorInvalidValue;  // G * B < 128: rejected by the interface
-        case 2: return launch_bwd_g<2, BW>(a, s);
-        case 4: return launch_bwd_g<4, BW>(a, s);
-        default: return launch_bwd_g<8, BW>(a, s);
+        case 2: return launch_bwd_g<D, 2, BW>(a, s);
+        case 4: return launch_bwd_g<D, 4, BW>(a, s);
+        default: return launch_bwd_g<D, 8, BW>(a, s);
     }
+}
+
+template <int D>
+hipError_t launch_bwd_d(const BwdArgs& a, hipStream_t s) {
+    return a.B == 64 ? launch_bwd_b<D, 64>(a, s) : launch_bwd_b<D, 128>(a, s);
 }
 
 }  // namespace
 
 hipError_t launch_backward(const BwdArgs& a, hipStream_t stream) {
-    if (a.B == 64) return launch_bwd_b<64>(a, stream);
-    return launch_bwd_b<128>(a, stream);
+    return a.head_dim == 64 ? launch_bwd_d<64>(a, stream) : launch_bwd_d<128>(a, stream);
 }
 
 }  // namespace bf1

@@ -24,7 +24,7 @@ struct AttnArgs {
     bool dense;             // implicit route {0..j} over 64-token blocks
 };
 
-// Backward (head_dim 128; G * B >= 128).  All pointers are device memory.
+// Backward (head_dim 64 or 128; G * B >= 128).  All pointers are device memory.
 struct BwdArgs {
     const void* Q;
     const void* K;
@@ -32,11 +32,11 @@ struct BwdArgs {
     const void* O;
     const void* dO;
     const float* LSE;
-    float* dQ;               // [batch, Hq, n, 128] fp32
-    float* dK;               // [batch, Hkv, n, 128] fp32
+    float* dQ;               // [batch, Hq, n, head_dim] fp32
+    float* dK;               // [batch, Hkv, n, head_dim] fp32
     float* dV;
     float* delta;            // workspace: [batch, Hq, n] fp32 (D = rowsum(dO * O))
-    float* part;             // workspace: [batch * Hkv, nslots, 2, 64, 128] fp32
+    float* part;             // workspace: [batch * Hkv, nslots, 2, 64, head_dim] fp32
     const int32_t* row_ptr;  // forward route (CSR)
     const int32_t* col_idx;
     int64_t nnz;
@@ -51,6 +51,7 @@ struct BwdArgs {
     int32_t Hq;
     int32_t Hkv;
     int32_t B;               // block width 64 or 128
+    int32_t head_dim;        // 64 or 128
 };
 
 hipError_t launch_backward(const BwdArgs& a, hipStream_t stream);

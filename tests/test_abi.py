@@ -124,6 +124,12 @@ def test_plan_transposed_matches_oracle(lib, n, B, L):
     assert ci.tolist() == ci_o.tolist()
 
 
+def test_bwd_workspace_size_head_dim_64(lib):
+    # partial dK/dV slots are 64 x head_dim fp32 tiles
+    D = (1 * 16 * 32768 * 4 + 255) // 256 * 256
+    assert bf1.bwd_workspace_size(1, 32768, 16, 8, 64, 64, 2) == D + 1 * 8 * 32 * 2 * 64 * 64 * 4
+
+
 def test_bwd_workspace_size(lib):
     # D (batch * Hq * n fp32, 256-byte rounded) plus the partial dK/dV slots of
     # the tiles whose query-block list is longer than one segment of 16: at
@@ -140,8 +146,8 @@ def test_backward_invalid_arguments_rejected_without_device(lib):
     args = [fake] * 9
     def call(*a, ws=fake, wsb=1 << 40):
         return lib.bf1_attn_bwd(*a, ws, wsb, None)
-    # head_dim 64 is not built for the backward
-    assert call(*args, 1, 128, 2, 1, 64, 64, 2) == bf1.BF1_ERR_UNSUPPORTED
+    # head_dims other than 64 and 128 are not built
+    assert call(*args, 1, 128, 2, 1, 96, 64, 2) == bf1.BF1_ERR_UNSUPPORTED
     # G * B < 128
     assert call(*args, 1, 128, 2, 2, 128, 64, 2) == bf1.BF1_ERR_UNSUPPORTED
     # missing gradient buffer / workspace, misaligned workspace, too small workspace

@@ -100,6 +100,42 @@ SMALL = [
 ]
 
 
+SMALL_D64 = [
+    # batch, n, Hq, Hkv, B, L  (head_dim 64)
+    (1, 512, 2, 1, 64, 1),       # the tiny workload's geometry
+    (2, 1000, 4, 2, 64, 2),      # ragged tail, batch 2
+    (1, 900, 2, 2, 128, 2),      # G = 1 with B = 128
+    (1, 2048, 16, 8, 64, 2),     # 16 / 8 heads
+    (1, 1, 2, 1, 64, 2),         # a single token
+    (1, 64 * 40, 8, 1, 64, 3),   # G = 8, key block 0's list split into segments
+]
+
+
+@pytest.mark.parametrize("cfg", SMALL_D64, ids=lambda c: "x".join(map(str, c)))
+def test_backward_head_dim_64_full_oracle(cfg):
+    batch, n, Hq, Hkv, B, L = cfg
+    say(f"backward d=64 {cfg}")
+    w = synth.Workload("bwd64", batch, n, Hq, Hkv, 64, B, L, seed=900 + n)
+    (dq, dk, dv), ref, terms = run_case(w)
+    for name, got, r, t in zip(("dQ", "dK", "dV"), (dq, dk, dv), ref, terms):
+        check_bound(got, r, t, tag=f"d64 {cfg} {name}")
+
+
+def test_backward_tiny_workload_chained():
+    # the tiny workload (n = 512, Hq 2, Hkv 1, d 64, L 1) through the GPU forward and backward
+    w = synth.WORKLOADS["tiny_n512"]
+    q, k, v = synth.make_qkv(w, device="cuda")
+    do = synth.make_grad_out(w, device="cuda")
+    o, lse = bf1.attn_fwd(q, k, v, w.b, w.L)
+    dq, dk, dv = bf1.attn_bwd(q, k, v, o, do, lse, w.b, w.L)
+    torch.cuda.synchronize()
+    ref = orc.attn_bwd_gathered_fp64(*(synth.to_f64(t) for t in (q, k, v, do)), w.b, w.L)
+    for name, got, r in zip(("dQ", "dK", "dV"), (dq, dk, dv), ref):
+        err = np.abs(got.cpu().double().numpy() - r).max()
+        say(f"  tiny chained {name}: max err {err:.3e} (max |ref| {np.abs(r).max():.3e})")
+        assert err <= 2e-2 * np.abs(r).max(), name
+
+
 @pytest.mark.parametrize("cfg", SMALL, ids=lambda c: "x".join(map(str, c)))
 def test_backward_small_full_oracle(cfg):
     batch, n, Hq, Hkv, B, L = cfg
