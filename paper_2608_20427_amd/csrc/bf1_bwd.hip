@@ -402,14 +402,28 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
 #pragma unroll
         for (int rh = 0; rh < 2; ++rh) {
             f32x16 s, dp;
+            // operand rows of this half issued as one group ahead of the
+            // MFMAs (left to itself the compiler serialises read, wait, MFMA)
+            u32x4 qa[BKS], oa[BKS];
 #pragma unroll
             for (int ks = 0; ks < BKS; ++ks) {
                 const int o = rw_off<D>(32 * rh + col, 2 * ks + half);
-                const u32x4 qa = *reinterpret_cast<const u32x4*>(qb + o);
-                const u32x4 oa = *reinterpret_cast<const u32x4*>(ob + o);
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, qa), kf[ks],
+                qa[ks] = *reinterpret_cast<const u32x4*>(qb + o);
+                oa[ks] = *reinterpret_cast<const u32x4*>(ob + o);
+            }
+            f32x4 l4s[4], d4s[4];
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+                const int rbase = 32 * rh + 8 * g4 + 4 * half;
+                l4s[g4] = *reinterpret_cast<const f32x4*>(&lse_s[buf][rbase]);
+                d4s[g4] = *reinterpret_cast<const f32x4*>(&del_s[buf][rbase]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int ks = 0; ks < BKS; ++ks) {
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, qa[ks]), kf[ks],
                                                             ks == 0 ? zero : s, 0, 0, 0);
-                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, oa), vf[ks],
+                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, oa[ks]), vf[ks],
                                                              ks == 0 ? zero : dp, 0, 0, 0);
             }
             // rows of this lane: 32 rh + 8 g4 + 4 half + c
@@ -417,8 +431,8 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
 #pragma unroll
             for (int g4 = 0; g4 < 4; ++g4) {
                 const int rbase = 32 * rh + 8 * g4 + 4 * half;
-                const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse_s[buf][rbase]);
-                const f32x4 d4 = *reinterpret_cast<const f32x4*>(&del_s[buf][rbase]);
+                const f32x4 l4 = l4s[g4];
+                const f32x4 d4 = d4s[g4];
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const int r = 4 * g4 + c;
@@ -429,8 +443,10 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
                     da[r >> 3][r & 7] = (__bf16)ds;
                 }
             }
+            // transpose reads of dO and Q for this half, as one group
+            u32x4 wo[BDT][2], wq[BDT][2];
 #pragma unroll
-            for (int dt = 0; dt < BDT; ++dt) {
+            for (int dt = 0; dt < BDT; ++dt)
 #pragma unroll
                 for (int m = 0; m < 2; ++m) {
                     const int go = 16 * (2 * rh + m) * BRB;
@@ -438,14 +454,19 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
                     const u32x2 ohi = lds_read_tr16(ol + tr_off<D>(lane, dt, 1) + go);
                     const u32x2 qlo = lds_read_tr16(ql + tr_off<D>(lane, dt, 0) + go);
                     const u32x2 qhi = lds_read_tr16(ql + tr_off<D>(lane, dt, 1) + go);
-                    const u32x4 wo = {olo[0], olo[1], ohi[0], ohi[1]};
-                    const u32x4 wq = {qlo[0], qlo[1], qhi[0], qhi[1]};
-                    dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa[m], __builtin_bit_cast(bf16x8, wo),
+                    wo[dt][m] = u32x4{olo[0], olo[1], ohi[0], ohi[1]};
+                    wq[dt][m] = u32x4{qlo[0], qlo[1], qhi[0], qhi[1]};
+                }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int dt = 0; dt < BDT; ++dt) {
+                    dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa[m], __builtin_bit_cast(bf16x8, wo[dt][m]),
                                                                      dv[dt], 0, 0, 0);
-                    dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da[m], __builtin_bit_cast(bf16x8, wq),
+                    dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da[m], __builtin_bit_cast(bf16x8, wq[dt][m]),
                                                                      dk[dt], 0, 0, 0);
                 }
-            }
         }
         __builtin_amdgcn_s_waitcnt(VMCNT0);  // this wave's loads of the next tile have landed
         __syncthreads();                      // ... and the other wave's; this tile is free
