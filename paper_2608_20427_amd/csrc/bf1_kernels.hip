@@ -362,10 +362,15 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
                     if (kp > qin) sc[kt][r] = -INFINITY;
                 }
         }
+        // maximum (not fmaxf): the scores are never NaN, and without NaN
+        // quieting the compiler emits three-input v_maximum3 directly instead
+        // of canonicalising every MFMA output first
         float mq[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};  // independent chains
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mq[r & 3] = fmaxf(mq[r & 3], fmaxf(sc[0][r], sc[1][r]));
-        m_cand = pair_max(fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]))) * c_log2;
+        for (int r = 0; r < 16; ++r)
+            mq[r & 3] = __builtin_elementwise_maximum(mq[r & 3], __builtin_elementwise_maximum(sc[0][r], sc[1][r]));
+        m_cand = pair_max(__builtin_elementwise_maximum(__builtin_elementwise_maximum(mq[0], mq[1]),
+                                                        __builtin_elementwise_maximum(mq[2], mq[3]))) * c_log2;
         return m_cand > m_run + RESCALE_LOG2;
     };
     auto apply_rescale = [&](bool need, float m_cand) {
