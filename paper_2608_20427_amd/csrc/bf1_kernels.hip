@@ -511,7 +511,9 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     // [row][16-byte chunk ^ (row % 16)], then reads back 16 consecutive bytes
     // per lane, 16 lanes per row, and stores 4 consecutive rows per
     // instruction.  The last step's barrier ordered every LDS read of the
-    // tiles before this; no other wave touches this slice.
+    // tiles before this; no other wave touches this slice.  The stores are
+    // non-temporal: O is not read again here, and streaming it through L2
+    // evicted K/V tiles that other workgroups were still reusing.
     const float l_tot = pair_sum(l_run);
     const float inv = 1.f / l_tot;
     constexpr int OCH = D / 8;                 // 16-byte chunks per row
@@ -536,7 +538,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
         for (int it = 0; it < 32 / RPI; ++it) {
             const int r = it * RPI + lane / OCH, c = lane % OCH;
             const u32x4 w = *reinterpret_cast<const u32x4*>(oslice + r * RB + ((c ^ (r % OCH)) * 16));
-            if (row0 + r < n) *reinterpret_cast<u32x4*>(Obase + (int64_t)r * D + c * 8) = w;
+            if (row0 + r < n) __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(Obase + (int64_t)r * D + c * 8));
         }
     }
     if (LSE != nullptr && half == 0 && qvalid)
