@@ -161,6 +161,9 @@ struct Unit {
     static_assert(NI >= 1 && KPW % RPI == 0, "page width and head_dim mismatch");
 };
 
+// K and V page rows are read once per decode step (a page is not shared
+// between the workgroups of a step), so the loads are non-temporal: they do
+// not displace other lines in L2.
 template <int D, int PW>
 __device__ __forceinline__ void load_unit(const __bf16* __restrict__ Kp, const __bf16* __restrict__ Vp,
                                           int64_t page_base, int quarter, int rg, int cch, u32x4* kr,
@@ -169,12 +172,12 @@ __device__ __forceinline__ void load_unit(const __bf16* __restrict__ Kp, const _
 #pragma unroll
     for (int i = 0; i < U::NI; ++i) {
         const int key = quarter * U::KPW + i * U::RPI + rg;
-        kr[i] = *reinterpret_cast<const u32x4*>(Kp + page_base + (int64_t)key * D + cch * 8);
+        kr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(Kp + page_base + (int64_t)key * D + cch * 8));
     }
 #pragma unroll
     for (int i = 0; i < U::NI; ++i) {
         const int key = quarter * U::KPW + i * U::RPI + rg;
-        vr[i] = *reinterpret_cast<const u32x4*>(Vp + page_base + (int64_t)key * D + cch * 8);
+        vr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(Vp + page_base + (int64_t)key * D + cch * 8));
     }
 }
 
