@@ -272,18 +272,33 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
     }
     __builtin_amdgcn_s_waitcnt(VMCNT0);
 
-    // ---- dQ = c dS K (rows past n are not stored) -----------------------------------
-    if (!qvalid) return;
-    float* drow = dQ + qrow * BD;
+    // ---- dQ = c dS K, staged through LDS into whole-row stores (rows past n skipped) ----
+    {
+        constexpr int QCH = BD / 4;  // 16-byte chunks per fp32 row
+        char* slice = wave == 0 ? reinterpret_cast<char*>(&kt_s[0][0])
+                    : wave == 1 ? reinterpret_cast<char*>(&kt_s[1][0])
+                    : wave == 2 ? reinterpret_cast<char*>(&vt_s[0][0])
+                                : reinterpret_cast<char*>(&vt_s[1][0]);
 #pragma unroll
-    for (int dt = 0; dt < BDT; ++dt)
+        for (int dt = 0; dt < BDT; ++dt)
 #pragma unroll
-        for (int gq4 = 0; gq4 < 4; ++gq4) {
-            f32x4 v4;
+            for (int gq4 = 0; gq4 < 4; ++gq4) {
+                f32x4 v4;
 #pragma unroll
-            for (int c = 0; c < 4; ++c) v4[c] = acc[dt][4 * gq4 + c] * scale;
-            *reinterpret_cast<f32x4*>(drow + 32 * dt + 8 * gq4 + 4 * half) = v4;
+                for (int c = 0; c < 4; ++c) v4[c] = acc[dt][4 * gq4 + c] * scale;
+                const int ch = (8 * dt + 2 * gq4 + half) ^ (col & 15);
+                *reinterpret_cast<f32x4*>(slice + col * (BD * 4) + ch * 16) = v4;
+            }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's dQ tile is in LDS
+        const int64_t row0 = qrow - col;      // first row of this wave
+        constexpr int RPI = 64 / QCH;         // rows per store instruction
+#pragma unroll
+        for (int it = 0; it < 32 / RPI; ++it) {
+            const int r = it * RPI + lane / QCH, c = lane % QCH;
+            const f32x4 w = *reinterpret_cast<const f32x4*>(slice + r * (BD * 4) + ((c ^ (r & 15)) * 16));
+            if (qpos - col + r < n) __builtin_nontemporal_store(w, reinterpret_cast<f32x4*>(dQ + (row0 + r) * BD + c * 4));
         }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -474,28 +489,47 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
     __builtin_amdgcn_s_waitcnt(VMCNT0);
 
     // ---- store: lane holds d column 32 dt + col, keys 8(r/4) + 4 half + r%4 ---------
-    // Directly into dK/dV (keys past n skipped) or into the segment's partial slot.
+    // Directly into dK/dV (keys past n skipped), staged through the idle query-tile
+    // buffers into whole-row non-temporal stores, or into the segment's partial slot.
+    if (slot < 0) {
+        constexpr int QCH = BD / 4;  // 16-byte chunks per fp32 row
+        char* sk = reinterpret_cast<char*>(wave == 0 ? &q_s[0][0] : &o_s[0][0]);
+        char* sv = reinterpret_cast<char*>(wave == 0 ? &q_s[1][0] : &o_s[1][0]);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int kl = 8 * (r >> 2) + 4 * half + (r & 3);  // key inside the wave's 32
+#pragma unroll
+            for (int dt = 0; dt < BDT; ++dt) {
+                const int off = kl * (BD * 4) + (((8 * dt + (col >> 2)) ^ (kl & 15)) * 16) + (col & 3) * 4;
+                *reinterpret_cast<float*>(sk + off) = dk[dt][r] * scale;
+                *reinterpret_cast<float*>(sv + off) = dv[dt][r];
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's tiles are in LDS
+        constexpr int RPI = 64 / QCH;         // rows per store instruction
+#pragma unroll
+        for (int it = 0; it < 32 / RPI; ++it) {
+            const int r = it * RPI + lane / QCH, c = lane % QCH;
+            const int off = r * (BD * 4) + ((c ^ (r & 15)) * 16);
+            const f32x4 wk = *reinterpret_cast<const f32x4*>(sk + off);
+            const f32x4 wv = *reinterpret_cast<const f32x4*>(sv + off);
+            const int32_t kp = i * BW + u * KT + 32 * wave + r;
+            if (kp < n) {
+                __builtin_nontemporal_store(wk, reinterpret_cast<f32x4*>(dK + (kvrow0 + kp) * BD + c * 4));
+                __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>(dV + (kvrow0 + kp) * BD + c * 4));
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
         const int key = 32 * wave + 8 * (r >> 2) + 4 * half + (r & 3);  // inside the 64-key tile
-        if (slot < 0) {
-            const int32_t kp = i * BW + u * KT + key;
-            if (kp >= n) continue;
-            float* krow = dK + (kvrow0 + kp) * BD;
-            float* vrow = dV + (kvrow0 + kp) * BD;
+        float* pk = part + (((int64_t)bh * nslots + slot) * 2) * (KT * BD) + key * BD;
+        float* pv = pk + KT * BD;
 #pragma unroll
-            for (int dt = 0; dt < BDT; ++dt) {
-                krow[32 * dt + col] = dk[dt][r] * scale;
-                vrow[32 * dt + col] = dv[dt][r];
-            }
-        } else {
-            float* pk = part + (((int64_t)bh * nslots + slot) * 2) * (KT * BD) + key * BD;
-            float* pv = pk + KT * BD;
-#pragma unroll
-            for (int dt = 0; dt < BDT; ++dt) {
-                pk[32 * dt + col] = dk[dt][r] * scale;
-                pv[32 * dt + col] = dv[dt][r];
-            }
+        for (int dt = 0; dt < BDT; ++dt) {
+            pk[32 * dt + col] = dk[dt][r] * scale;
+            pv[32 * dt + col] = dv[dt][r];
         }
     }
 }
