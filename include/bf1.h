@@ -150,7 +150,7 @@ int bf1_plan_transposed(int64_t n, int32_t B, int32_t L,
  *              contents on entry are irrelevant and are clobbered.
  * Supported: head_dim in {64, 128}, B in {64, 128}, G = Hq/Hkv in {1, 2, 4, 8}
  * with G * B >= 128 (so G = 1 needs B = 128); others return BF1_ERR_UNSUPPORTED.
- * Three kernels on `stream`: dQ (also writes D to the workspace), dK/dV
+ * Three kernels on `stream`: dQ (also writes D and LSE log2 e to the workspace), dK/dV
  * over the transposed route (cut into segments of at most 16 query blocks;
  * the segments of long lists -- block 0 -- leave partial sums in the
  * workspace), and a fixed-order sum of those partials.  The route and its

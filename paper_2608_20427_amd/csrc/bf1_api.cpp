@@ -209,7 +209,7 @@ int bwd_workspace_bytes(int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32
     if (!bwd_layout(n, B, L, &lay, false)) return BF1_ERR_INVALID_ARG;
     const int64_t delta = ((int64_t)batch * Hq * n * 4 + 255) / 256 * 256;
     const int64_t part = (int64_t)batch * Hkv * lay.nslots * 2 * 64 * head_dim * 4;
-    *bytes = delta + part;
+    *bytes = 2 * delta + part;  // D, LSE * log2 e, partial tiles
     return BF1_OK;
 }
 
@@ -465,8 +465,9 @@ int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, con
     if (st != BF1_OK) return st;
     const int64_t delta_bytes = ((int64_t)batch * Hq * n * 4 + 255) / 256 * 256;
     float* delta = (float*)workspace;
-    float* part = (float*)((char*)workspace + delta_bytes);
-    bf1::BwdArgs a{Q, K, V, O, dO, LSE, dQ, dK, dV, delta, part,
+    float* lse2 = (float*)((char*)workspace + delta_bytes);
+    float* part = (float*)((char*)workspace + 2 * delta_bytes);
+    bf1::BwdArgs a{Q, K, V, O, dO, LSE, dQ, dK, dV, delta, lse2, part,
                    plan.row_ptr, plan.col_idx, plan.nnz, bp.users, bp.segs, bp.nseg,
                    bp.reds, bp.nred, bp.nslots, batch, n, Hq, Hkv, B, head_dim};
     return status_of(bf1::launch_backward(a, s));

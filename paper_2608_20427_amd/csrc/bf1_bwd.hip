@@ -8,7 +8,7 @@
 // Kernels:
 //  * bwd_dq_kernel   -- one workgroup per (batch, kv-head, query block, row
 //    chunk), walking the forward route like the forward kernel; computes D
-//    for its rows (written for the next kernel) and dQ.
+//    and LSE log2 e for its rows (written for the next kernel) and dQ.
 //  * bwd_dkdv_kernel -- one workgroup per (batch, kv-head, 64-key tile,
 //    segment of the tile's query-block list), walking the TRANSPOSED route
 //    (the query blocks that select the key block); accumulates dK and dV in
@@ -94,7 +94,8 @@ template <int D, int G, int BW, bool DENSE>
 __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ O, const __bf16* __restrict__ dO, const float* __restrict__ LSE,
-    float* __restrict__ dQ, float* __restrict__ Delta, const int32_t* __restrict__ row_ptr,
+    float* __restrict__ dQ, float* __restrict__ Delta, float* __restrict__ Lse2,
+    const int32_t* __restrict__ row_ptr,
     const int32_t* __restrict__ col_idx, int64_t nnz, int32_t n, int32_t NB, int32_t batch_hkv,
     int32_t Hkv, float c_log2, float scale) {
     BWD_GEOMETRY(D);
@@ -150,8 +151,11 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
         }
     }
     const float Dq = pair_sum(dpart);  // the two lane halves hold the two halves of d
-    if (qvalid && half == 0) Delta[qrow] = Dq;
     const float lse2 = qvalid ? LSE[qrow] * LOG2E : INFINITY;  // rows past n: P = 0
+    if (qvalid && half == 0) {  // D and LSE log2 e of the row, for the dK/dV kernel
+        Delta[qrow] = Dq;
+        Lse2[qrow] = lse2;
+    }
 
     // ---- route walk (as in the forward) -------------------------------------------
     int32_t pos_end, cur_p;
@@ -307,7 +311,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
 // Workgroup = 2 waves; wave w owns keys 32 w .. 32 w + 31 of one 64-key tile
 // (block i, sub-tile u) and holds their K^T and V^T as MFMA B operands in
 // registers.  It walks query tiles (64 rows of one q-head of a query block j
-// that selects block i), staged in LDS: Q and dO rows, LSE and D.  Per 32-row
+// that selects block i), staged in LDS: Q and dO rows, LSE log2 e and D.  Per 32-row
 // half of a query tile:
 //   S = Q K^T, dP = dO V^T          (A: row-wise reads of the Q / dO tiles)
 //   P = exp2(c log2e S - log2e LSE), dS = P (dP - D)   (lane = key column)
@@ -319,7 +323,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
 template <int D, int G, int BW>
 __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
-    const __bf16* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ Delta,
+    const __bf16* __restrict__ dO, const float* __restrict__ Lse2, const float* __restrict__ Delta,
     float* __restrict__ dK, float* __restrict__ dV, float* __restrict__ part,
     const int32_t* __restrict__ segs, const int32_t* __restrict__ users, int32_t nslots,
     int32_t n, int32_t batch_hkv, int32_t Hkv, float c_log2, float scale) {
@@ -389,8 +393,8 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
             load_lds_async<16>(qr, &q_s[buf][seg * 64], seg_off<D>(seg, lane), soff);
             load_lds_async<16>(orr, &o_s[buf][seg * 64], seg_off<D>(seg, lane), soff);
         }
-        // 64 rows of LSE (wave 0) or D (wave 1), 4 bytes per lane
-        const float* src = (wave == 0 ? LSE : Delta) + qr0;
+        // 64 rows of LSE log2 e (wave 0) or D (wave 1), 4 bytes per lane
+        const float* src = (wave == 0 ? Lse2 : Delta) + qr0;
         float* dst = wave == 0 ? &lse_s[buf][0] : &del_s[buf][0];
         load_lds_async<4>(head_rsrc(src, (uint32_t)n * 4), dst, (uint32_t)lane * 4, (uint32_t)row0 * 4);
     };
@@ -443,21 +447,27 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
             }
             // rows of this lane: 32 rh + 8 g4 + 4 half + c
             bf16x8 pa[2], da[2];
+            float pr[16];
 #pragma unroll
-            for (int g4 = 0; g4 < 4; ++g4) {
-                const int rbase = 32 * rh + 8 * g4 + 4 * half;
-                const f32x4 l4 = l4s[g4];
-                const f32x4 d4 = d4s[g4];
+            for (int g4 = 0; g4 < 4; ++g4)
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    pr[4 * g4 + c] = __builtin_amdgcn_exp2f(fmaf(s[4 * g4 + c], c_log2, -l4s[g4][c]));
+            if (self) {  // the key-block-diagonal tile: token-level causal mask
+#pragma unroll
+                for (int g4 = 0; g4 < 4; ++g4)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        if (kin > qsub + 32 * rh + 8 * g4 + 4 * half + c) pr[4 * g4 + c] = 0.f;
+            }
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4)
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const int r = 4 * g4 + c;
-                    float p = __builtin_amdgcn_exp2f(fmaf(s[r], c_log2, -l4[c] * LOG2E));
-                    if (self && kin > qsub + rbase + c) p = 0.f;
-                    const float ds = p * (dp[r] - d4[c]);
-                    pa[r >> 3][r & 7] = (__bf16)p;
-                    da[r >> 3][r & 7] = (__bf16)ds;
+                    pa[r >> 3][r & 7] = (__bf16)pr[r];
+                    da[r >> 3][r & 7] = (__bf16)(pr[r] * (dp[r] - d4s[g4][c]));
                 }
-            }
             // transpose reads of dO and Q for this half, as one group
             u32x4 wo[BDT][2], wq[BDT][2];
 #pragma unroll
@@ -582,14 +592,14 @@ hipError_t launch_bwd_g(const BwdArgs& a, hipStream_t stream) {
     const float c_log2 = scale * LOG2E;
     hipLaunchKernelGGL((bwd_dq_kernel<D, G, BW, false>), dim3((unsigned)items), dim3(256), 0, stream,
                        (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, (const __bf16*)a.O,
-                       (const __bf16*)a.dO, a.LSE, a.dQ, a.delta, a.row_ptr, a.col_idx, a.nnz,
+                       (const __bf16*)a.dO, a.LSE, a.dQ, a.delta, a.lse2, a.row_ptr, a.col_idx, a.nnz,
                        (int32_t)a.n, NB, bhk, a.Hkv, c_log2, scale);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.nseg > 0) {
         hipLaunchKernelGGL((bwd_dkdv_kernel<D, G, BW>), dim3((unsigned)(a.nseg * bhk)), dim3(128), 0,
                            stream, (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
-                           (const __bf16*)a.dO, a.LSE, a.delta, a.dK, a.dV, a.part, a.segs,
+                           (const __bf16*)a.dO, a.lse2, a.delta, a.dK, a.dV, a.part, a.segs,
                            a.users, a.nslots, (int32_t)a.n, bhk, a.Hkv, c_log2, scale);
         e = hipGetLastError();
         if (e != hipSuccess) return e;

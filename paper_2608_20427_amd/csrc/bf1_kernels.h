@@ -36,6 +36,7 @@ struct BwdArgs {
     float* dK;               // [batch, Hkv, n, head_dim] fp32
     float* dV;
     float* delta;            // workspace: [batch, Hq, n] fp32 (D = rowsum(dO * O))
+    float* lse2;             // workspace: [batch, Hq, n] fp32 (LSE * log2 e)
     float* part;             // workspace: [batch * Hkv, nslots, 2, 64, head_dim] fp32
     const int32_t* row_ptr;  // forward route (CSR)
     const int32_t* col_idx;

@@ -127,18 +127,19 @@ def test_plan_transposed_matches_oracle(lib, n, B, L):
 def test_bwd_workspace_size_head_dim_64(lib):
     # partial dK/dV slots are 64 x head_dim fp32 tiles
     D = (1 * 16 * 32768 * 4 + 255) // 256 * 256
-    assert bf1.bwd_workspace_size(1, 32768, 16, 8, 64, 64, 2) == D + 1 * 8 * 32 * 2 * 64 * 64 * 4
+    assert bf1.bwd_workspace_size(1, 32768, 16, 8, 64, 64, 2) == 2 * D + 1 * 8 * 32 * 2 * 64 * 64 * 4
 
 
 def test_bwd_workspace_size(lib):
-    # D (batch * Hq * n fp32, 256-byte rounded) plus the partial dK/dV slots of
-    # the tiles whose query-block list is longer than one segment of 16: at
-    # 32K / b = 64 only block 0 (512 users -> 32 segments).
+    # D and LSE log2 e (each batch * Hq * n fp32, 256-byte rounded) plus the
+    # partial dK/dV slots of the tiles whose query-block list is longer than
+    # one segment of 16: at 32K / b = 64 only block 0 (512 users -> 32
+    # segments).
     D = (1 * 16 * 32768 * 4 + 255) // 256 * 256
     part = 1 * 8 * 32 * 2 * 64 * 128 * 4
-    assert bf1.bwd_workspace_size(1, 32768, 16, 8, 128, 64, 2) == D + part
+    assert bf1.bwd_workspace_size(1, 32768, 16, 8, 128, 64, 2) == 2 * D + part
     # a short sequence has no split lists
-    assert bf1.bwd_workspace_size(1, 512, 2, 1, 128, 64, 1) == (2 * 512 * 4 + 255) // 256 * 256
+    assert bf1.bwd_workspace_size(1, 512, 2, 1, 128, 64, 1) == 2 * ((2 * 512 * 4 + 255) // 256 * 256)
 
 
 def test_backward_invalid_arguments_rejected_without_device(lib):
