@@ -241,16 +241,23 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
             }
         // dS^T = P^T (dP^T - D), packed as the B operands of K^T dS^T
         bf16x8 db[4];
-        const bool self = ti == j;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) st[kt][r] = __builtin_amdgcn_exp2f(fmaf(st[kt][r], c_log2, -lse2));
+        if (ti == j) {  // the key-block-diagonal tile: token-level causal mask
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    if (tu * KT + 32 * kt + 8 * (r >> 2) + 4 * half + (r & 3) > qin) st[kt][r] = 0.f;
+        }
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
             f32x8 v8;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int kp = tu * KT + 32 * kt + 8 * (r >> 2) + 4 * half + (r & 3);
-                float p = __builtin_amdgcn_exp2f(fmaf(st[kt][r], c_log2, -lse2));
-                if (self && kp > qin) p = 0.f;
-                v8[r & 7] = p * (dpt[kt][r] - Dq);
+                v8[r & 7] = st[kt][r] * (dpt[kt][r] - Dq);
                 if ((r & 7) == 7) db[2 * kt + (r >> 3)] = __builtin_convertvector(v8, bf16x8);
             }
         }
