@@ -553,36 +553,49 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
 
 // Sum of the partial slots of split key tiles: reduce descriptor (int32 x 4) =
 // key block, sub-tile, first slot, slot count.  Fixed summation order.  One
-// workgroup per (descriptor, batch x kv-head, 512-element chunk of the 64 x 128
-// tile); each thread sums two elements of dK and of dV over the slots.
-constexpr int RED_CHUNK = 512;
+// workgroup per (descriptor, batch x kv-head, 256-element chunk of the 64 x D
+// tile); each thread sums one element of dK and of dV over the slots.
+constexpr int RED_CHUNK = 256;
 template <int D, int BW>
 __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     float* __restrict__ dK, float* __restrict__ dV, const float* __restrict__ part,
     const int32_t* __restrict__ reds, int32_t nslots, int32_t n, int32_t batch_hkv) {
     BWD_GEOMETRY(D);
     constexpr int NCH = KT * BD / RED_CHUNK;
+    constexpr int64_t SLOT = 2 * KT * BD;  // floats per slot (dK tile, then dV tile)
     const int32_t x = blockIdx.x;
     const int ch = x % NCH;
     const int32_t bh = (x / NCH) % batch_hkv;
     const int32_t* rd = reds + 4 * (x / NCH / batch_hkv);
     const int32_t i = rd[0], u = rd[1], s0 = rd[2], ns = rd[3];
     const int64_t kvrow0 = (int64_t)bh * n;
+    const int e = ch * RED_CHUNK + threadIdx.x;  // element of the 64 x D tile
+    const int key = e / BD, d = e % BD;
+    const int32_t kp = i * BW + u * KT + key;
+    const float* pk = part + ((int64_t)bh * nslots + s0) * SLOT + e;
+    // slots summed in order; eight slots' loads are issued before their sums
+    float sk = 0.f, sv = 0.f;
+    int32_t s = 0;
+    for (; s + 8 <= ns; s += 8) {
+        float kk[8], vv[8];
 #pragma unroll
-    for (int h = 0; h < RED_CHUNK / 256; ++h) {
-        const int e = ch * RED_CHUNK + h * 256 + threadIdx.x;
-        const int key = e / BD, d = e % BD;
-        const int32_t kp = i * BW + u * KT + key;
-        float sk = 0.f, sv = 0.f;
-        for (int32_t s = 0; s < ns; ++s) {
-            const float* pk = part + (((int64_t)bh * nslots + s0 + s) * 2) * (KT * BD);
-            sk += pk[e];
-            sv += pk[KT * BD + e];
+        for (int q = 0; q < 8; ++q) {
+            kk[q] = pk[(s + q) * SLOT];
+            vv[q] = pk[(s + q) * SLOT + KT * BD];
         }
-        if (kp < n) {
-            dK[(kvrow0 + kp) * BD + d] = sk;
-            dV[(kvrow0 + kp) * BD + d] = sv;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            sk += kk[q];
+            sv += vv[q];
         }
+    }
+    for (; s < ns; ++s) {
+        sk += pk[s * SLOT];
+        sv += pk[s * SLOT + KT * BD];
+    }
+    if (kp < n) {
+        dK[(kvrow0 + kp) * BD + d] = sk;
+        dV[(kvrow0 + kp) * BD + d] = sv;
     }
 }
 
