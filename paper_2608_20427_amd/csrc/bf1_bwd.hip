@@ -315,38 +315,46 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
 // ---------------------------------------------------------------------------
 // dK, dV
 // ---------------------------------------------------------------------------
-// Workgroup = 2 waves; wave w owns keys 32 w .. 32 w + 31 of one 64-key tile
-// (block i, sub-tile u) and holds their K^T and V^T as MFMA B operands in
-// registers.  It walks query tiles (64 rows of one q-head of a query block j
-// that selects block i), staged in LDS: Q and dO rows, LSE log2 e and D.  Per 32-row
-// half of a query tile:
-//   S = Q K^T, dP = dO V^T          (A: row-wise reads of the Q / dO tiles)
-//   P = exp2(c log2e S - log2e LSE), dS = P (dP - D)   (lane = key column)
-//   dV += P^T dO, dK += dS^T Q      (A: P / dS packed from the lane's own
-//                                    registers; B: transpose reads of dO / Q)
-// A segment descriptor (int32 x 8): key block, sub-tile, first entry of its
-// query-block list in the transposed table, entry count, partial slot (-1:
-// write dK/dV directly).
+// Workgroup = 4 waves over one 64-key tile (block i, sub-tile u).  Waves 0
+// and 1 ("P waves") own keys 0..31 and 32..63 for S, P and dV and hold their
+// K^T as MFMA B operands in registers; waves 2 and 3 ("dS waves") own the same
+// keys for dP, dS and dK and hold their V^T.  The workgroup walks query tiles
+// (64 rows of one q-head of a query block j that selects block i), staged in
+// LDS: Q and dO rows, LSE log2 e and D.  Per 32-row half of a query tile:
+//   phase 1: S = Q K^T (P waves) or dP = dO V^T (dS waves)  (A: row-wise reads)
+//            P waves: P = exp2(c log2e S - log2e LSE), to LDS (fp32)
+//   phase 2: dS waves read P; dS = P (dP - D)                (lane = key column)
+//   phase 3: dV += P^T dO (P waves) or dK += dS^T Q (dS waves)
+//            (A: P / dS packed from the lane's own registers; B: transpose reads)
+// Splitting the roles halves each wave's registers (no accumulator leaves the
+// VGPRs) and gives two workgroups, two waves per SIMD, per CU.  Two barriers
+// per half order the exchange of P.  A segment descriptor (int32 x 8): key
+// block, sub-tile, first entry of its query-block list in the transposed
+// table, entry count, partial slot (-1: write dK/dV directly).
 template <int D, int G, int BW>
-__global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(256, 2) void bwd_dkdv_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float* __restrict__ Lse2, const float* __restrict__ Delta,
     float* __restrict__ dK, float* __restrict__ dV, float* __restrict__ part,
     const int32_t* __restrict__ segs, const int32_t* __restrict__ users, int32_t nslots,
     int32_t n, int32_t batch_hkv, int32_t Hkv, float c_log2, float scale) {
     BWD_GEOMETRY(D);
-    constexpr int NW = 2;
+    constexpr int NW = 4;
     constexpr int NSUB = BW / KT;
     constexpr int SPW = (BTILE / 1024) / NW;  // Q (or dO) segments per wave per tile
+    static_assert(SPW * NW * 1024 == BTILE, "segments must split over the waves");
 
     __shared__ u32x4 q_s[2][BTILE / 16];
     __shared__ u32x4 o_s[2][BTILE / 16];
     __shared__ float lse_s[2][KT];
     __shared__ float del_s[2][KT];
+    __shared__ f32x4 p_x[2][4][64];  // P of the current half: [key half][row group][lane]
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int kw = wave & 1;   // key half of the tile
+    const bool pw = wave < 2;  // P wave (S, P, dV) or dS wave (dP, dS, dK)
     const int col = lane & 31;
     const int half = lane >> 5;
 
@@ -362,24 +370,19 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
     const int32_t g = bh % Hkv;
     const int Hq = Hkv * G;
 
-    const int kin = u * KT + 32 * wave + col;  // key position inside block i of this lane's column
+    const int kin = u * KT + 32 * kw + col;  // key position inside block i of this lane's column
     const int32_t kpos = i * BW + kin;
     const int64_t kvrow0 = ((int64_t)beta * Hkv + g) * (int64_t)n;
 
-    // ---- K^T and V^T of this wave's 32 keys (B operands), zero past n ---------------
-    bf16x8 kf[BKS], vf[BKS];
+    // ---- K^T (P waves) or V^T (dS waves) of this wave's 32 keys, zero past n -------
+    bf16x8 bop[BKS];
     {
-        const u32x4* ks = reinterpret_cast<const u32x4*>(K + (kvrow0 + kpos) * BD);
-        const u32x4* vs = reinterpret_cast<const u32x4*>(V + (kvrow0 + kpos) * BD);
+        const u32x4* src = reinterpret_cast<const u32x4*>((pw ? K : V) + (kvrow0 + kpos) * BD);
 #pragma unroll
         for (int s = 0; s < BKS; ++s) {
-            u32x4 wk = {0u, 0u, 0u, 0u}, wv = wk;
-            if (kpos < n) {
-                wk = ks[2 * s + half];
-                wv = vs[2 * s + half];
-            }
-            kf[s] = __builtin_bit_cast(bf16x8, wk);
-            vf[s] = __builtin_bit_cast(bf16x8, wv);
+            u32x4 w = {0u, 0u, 0u, 0u};
+            if (kpos < n) w = src[2 * s + half];
+            bop[s] = __builtin_bit_cast(bf16x8, w);
         }
     }
 
@@ -401,17 +404,19 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
             load_lds_async<16>(orr, &o_s[buf][seg * 64], seg_off<D>(seg, lane), soff);
         }
         // 64 rows of LSE log2 e (wave 0) or D (wave 1), 4 bytes per lane
-        const float* src = (wave == 0 ? Lse2 : Delta) + qr0;
-        float* dst = wave == 0 ? &lse_s[buf][0] : &del_s[buf][0];
-        load_lds_async<4>(head_rsrc(src, (uint32_t)n * 4), dst, (uint32_t)lane * 4, (uint32_t)row0 * 4);
+        if (wave < 2) {
+            const float* src = (wave == 0 ? Lse2 : Delta) + qr0;
+            float* dst = wave == 0 ? &lse_s[buf][0] : &del_s[buf][0];
+            load_lds_async<4>(head_rsrc(src, (uint32_t)n * 4), dst, (uint32_t)lane * 4, (uint32_t)row0 * 4);
+        }
     };
     auto tile_query_block = [&](int32_t t) -> int32_t { return users[uoff + t / (G * NSUB)]; };
 
-    f32x16 dk[BDT], dv[BDT];
+    f32x16 acc[BDT];  // dV (P waves) or dK / scale (dS waves)
 #pragma unroll
     for (int t = 0; t < BDT; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) dk[t][r] = dv[t][r] = 0.f;
+        for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
 
     if (ntiles > 0) stage(0, 0);
     __builtin_amdgcn_s_waitcnt(VMCNT0);
@@ -422,132 +427,126 @@ __global__ __launch_bounds__(128, 1) void bwd_dkdv_kernel(
         const int32_t jq = tile_query_block(t);
         const bool self = jq == i;
         const int qsub = (t % NSUB) * KT;  // query position of tile row 0 inside block jq
-        const char* qb = reinterpret_cast<const char*>(&q_s[buf][0]);
-        const char* ob = reinterpret_cast<const char*>(&o_s[buf][0]);
-        const uint32_t ql = lds_addr(qb), ol = lds_addr(ob);
+        // phase-1 rows (Q for S, dO for dP); phase-3 transposed tile (dO for dV, Q for dK)
+        const char* ab = reinterpret_cast<const char*>(pw ? &q_s[buf][0] : &o_s[buf][0]);
+        const uint32_t tl = lds_addr(pw ? &o_s[buf][0] : &q_s[buf][0]);
+        const float* rvs = pw ? &lse_s[buf][0] : &del_s[buf][0];
 #pragma unroll
         for (int rh = 0; rh < 2; ++rh) {
-            f32x16 s, dp;
-            // operand rows of this half issued as one group ahead of the
-            // MFMAs (left to itself the compiler serialises read, wait, MFMA)
-            u32x4 qa[BKS], oa[BKS];
+            // ---- phase 1: operand rows of this half issued as one group ahead of
+            // the MFMAs (left to itself the compiler serialises read, wait, MFMA)
+            u32x4 opa[BKS];
 #pragma unroll
-            for (int ks = 0; ks < BKS; ++ks) {
-                const int o = rw_off<D>(32 * rh + col, 2 * ks + half);
-                qa[ks] = *reinterpret_cast<const u32x4*>(qb + o);
-                oa[ks] = *reinterpret_cast<const u32x4*>(ob + o);
-            }
-            f32x4 l4s[4], d4s[4];
-#pragma unroll
-            for (int g4 = 0; g4 < 4; ++g4) {
-                const int rbase = 32 * rh + 8 * g4 + 4 * half;
-                l4s[g4] = *reinterpret_cast<const f32x4*>(&lse_s[buf][rbase]);
-                d4s[g4] = *reinterpret_cast<const f32x4*>(&del_s[buf][rbase]);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int ks = 0; ks < BKS; ++ks) {
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, qa[ks]), kf[ks],
-                                                            ks == 0 ? zero : s, 0, 0, 0);
-                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, oa[ks]), vf[ks],
-                                                             ks == 0 ? zero : dp, 0, 0, 0);
-            }
-            // rows of this lane: 32 rh + 8 g4 + 4 half + c
-            bf16x8 pa[2], da[2];
-            float pr[16];
+            for (int ks = 0; ks < BKS; ++ks)
+                opa[ks] = *reinterpret_cast<const u32x4*>(ab + rw_off<D>(32 * rh + col, 2 * ks + half));
+            f32x4 rv[4];  // LSE log2 e (P waves) or D (dS waves) of the lane's rows
 #pragma unroll
             for (int g4 = 0; g4 < 4; ++g4)
+                rv[g4] = *reinterpret_cast<const f32x4*>(rvs + 32 * rh + 8 * g4 + 4 * half);
+            __builtin_amdgcn_sched_barrier(0);
+            f32x16 sc;
 #pragma unroll
-                for (int c = 0; c < 4; ++c)
-                    pr[4 * g4 + c] = __builtin_amdgcn_exp2f(fmaf(s[4 * g4 + c], c_log2, -l4s[g4][c]));
-            if (self) {  // the key-block-diagonal tile: token-level causal mask
+            for (int ks = 0; ks < BKS; ++ks)
+                sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, opa[ks]), bop[ks],
+                                                             ks == 0 ? zero : sc, 0, 0, 0);
+            // rows of this lane: 32 rh + 8 g4 + 4 half + c
+            bf16x8 pk2[2];
+            if (pw) {
+                float pr[16];
 #pragma unroll
                 for (int g4 = 0; g4 < 4; ++g4)
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
-                        if (kin > qsub + 32 * rh + 8 * g4 + 4 * half + c) pr[4 * g4 + c] = 0.f;
-            }
+                        pr[4 * g4 + c] = __builtin_amdgcn_exp2f(fmaf(sc[4 * g4 + c], c_log2, -rv[g4][c]));
+                if (self) {  // the key-block-diagonal tile: token-level causal mask
 #pragma unroll
-            for (int g4 = 0; g4 < 4; ++g4)
+                    for (int g4 = 0; g4 < 4; ++g4)
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const int r = 4 * g4 + c;
-                    pa[r >> 3][r & 7] = (__bf16)pr[r];
-                    da[r >> 3][r & 7] = (__bf16)(pr[r] * (dp[r] - d4s[g4][c]));
+                        for (int c = 0; c < 4; ++c)
+                            if (kin > qsub + 32 * rh + 8 * g4 + 4 * half + c) pr[4 * g4 + c] = 0.f;
                 }
-            // transpose reads of dO and Q for this half, as one group
-            u32x4 wo[BDT][2], wq[BDT][2];
+#pragma unroll
+                for (int g4 = 0; g4 < 4; ++g4)
+                    p_x[kw][g4][lane] = f32x4{pr[4 * g4], pr[4 * g4 + 1], pr[4 * g4 + 2], pr[4 * g4 + 3]};
+#pragma unroll
+                for (int r = 0; r < 16; ++r) pk2[r >> 3][r & 7] = (__bf16)pr[r];
+            }
+            __syncthreads();  // P of this half is in LDS
+            // ---- phase 2: the dS waves take P
+            f32x4 pp[4];
+            if (!pw) {
+#pragma unroll
+                for (int g4 = 0; g4 < 4; ++g4) pp[g4] = p_x[kw][g4][lane];
+            }
+            __syncthreads();  // ... and has been read: the exchange buffer is free again
+            if (!pw) {
+#pragma unroll
+                for (int g4 = 0; g4 < 4; ++g4)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        const int r = 4 * g4 + c;
+                        pk2[r >> 3][r & 7] = (__bf16)(pp[g4][c] * (sc[r] - rv[g4][c]));
+                    }
+            }
+            // ---- phase 3: transpose reads of dO (P waves) or Q (dS waves), as one group
+            u32x4 wt[BDT][2];
 #pragma unroll
             for (int dt = 0; dt < BDT; ++dt)
 #pragma unroll
                 for (int m = 0; m < 2; ++m) {
                     const int go = 16 * (2 * rh + m) * BRB;
-                    const u32x2 olo = lds_read_tr16(ol + tr_off<D>(lane, dt, 0) + go);
-                    const u32x2 ohi = lds_read_tr16(ol + tr_off<D>(lane, dt, 1) + go);
-                    const u32x2 qlo = lds_read_tr16(ql + tr_off<D>(lane, dt, 0) + go);
-                    const u32x2 qhi = lds_read_tr16(ql + tr_off<D>(lane, dt, 1) + go);
-                    wo[dt][m] = u32x4{olo[0], olo[1], ohi[0], ohi[1]};
-                    wq[dt][m] = u32x4{qlo[0], qlo[1], qhi[0], qhi[1]};
+                    const u32x2 lo = lds_read_tr16(tl + tr_off<D>(lane, dt, 0) + go);
+                    const u32x2 hi = lds_read_tr16(tl + tr_off<D>(lane, dt, 1) + go);
+                    wt[dt][m] = u32x4{lo[0], lo[1], hi[0], hi[1]};
                 }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int m = 0; m < 2; ++m)
 #pragma unroll
-                for (int dt = 0; dt < BDT; ++dt) {
-                    dv[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa[m], __builtin_bit_cast(bf16x8, wo[dt][m]),
-                                                                     dv[dt], 0, 0, 0);
-                    dk[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(da[m], __builtin_bit_cast(bf16x8, wq[dt][m]),
-                                                                     dk[dt], 0, 0, 0);
-                }
+                for (int dt = 0; dt < BDT; ++dt)
+                    acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pk2[m], __builtin_bit_cast(bf16x8, wt[dt][m]),
+                                                                      acc[dt], 0, 0, 0);
         }
         __builtin_amdgcn_s_waitcnt(VMCNT0);  // this wave's loads of the next tile have landed
-        __syncthreads();                      // ... and the other wave's; this tile is free
+        __syncthreads();                      // ... and the other waves'; this tile is free
     }
     __builtin_amdgcn_s_waitcnt(VMCNT0);
 
     // ---- store: lane holds d column 32 dt + col, keys 8(r/4) + 4 half + r%4 ---------
-    // Directly into dK/dV (keys past n skipped), staged through the idle query-tile
-    // buffers into whole-row non-temporal stores, or into the segment's partial slot.
+    // dV (P waves) or dK (dS waves) directly (keys past n skipped), staged through
+    // the idle query-tile buffers into whole-row non-temporal stores, or into the
+    // segment's partial slot.
+    const float osc = pw ? 1.f : scale;
     if (slot < 0) {
         constexpr int QCH = BD / 4;  // 16-byte chunks per fp32 row
-        char* sk = reinterpret_cast<char*>(wave == 0 ? &q_s[0][0] : &o_s[0][0]);
-        char* sv = reinterpret_cast<char*>(wave == 0 ? &q_s[1][0] : &o_s[1][0]);
+        char* st = reinterpret_cast<char*>(wave < 2 ? &q_s[wave][0] : &o_s[wave - 2][0]);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int kl = 8 * (r >> 2) + 4 * half + (r & 3);  // key inside the wave's 32
 #pragma unroll
             for (int dt = 0; dt < BDT; ++dt) {
                 const int off = kl * (BD * 4) + (((8 * dt + (col >> 2)) ^ (kl & 15)) * 16) + (col & 3) * 4;
-                *reinterpret_cast<float*>(sk + off) = dk[dt][r] * scale;
-                *reinterpret_cast<float*>(sv + off) = dv[dt][r];
+                *reinterpret_cast<float*>(st + off) = acc[dt][r] * osc;
             }
         }
-        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's tiles are in LDS
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's tile is in LDS
+        float* out = pw ? dV : dK;
         constexpr int RPI = 64 / QCH;         // rows per store instruction
 #pragma unroll
         for (int it = 0; it < 32 / RPI; ++it) {
             const int r = it * RPI + lane / QCH, c = lane % QCH;
-            const int off = r * (BD * 4) + ((c ^ (r & 15)) * 16);
-            const f32x4 wk = *reinterpret_cast<const f32x4*>(sk + off);
-            const f32x4 wv = *reinterpret_cast<const f32x4*>(sv + off);
-            const int32_t kp = i * BW + u * KT + 32 * wave + r;
-            if (kp < n) {
-                __builtin_nontemporal_store(wk, reinterpret_cast<f32x4*>(dK + (kvrow0 + kp) * BD + c * 4));
-                __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>(dV + (kvrow0 + kp) * BD + c * 4));
-            }
+            const f32x4 w = *reinterpret_cast<const f32x4*>(st + r * (BD * 4) + ((c ^ (r & 15)) * 16));
+            const int32_t kp = i * BW + u * KT + 32 * kw + r;
+            if (kp < n) __builtin_nontemporal_store(w, reinterpret_cast<f32x4*>(out + (kvrow0 + kp) * BD + c * 4));
         }
         return;
     }
+    float* dst = part + (((int64_t)bh * nslots + slot) * 2 + (pw ? 1 : 0)) * (KT * BD);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-        const int key = 32 * wave + 8 * (r >> 2) + 4 * half + (r & 3);  // inside the 64-key tile
-        float* pk = part + (((int64_t)bh * nslots + slot) * 2) * (KT * BD) + key * BD;
-        float* pv = pk + KT * BD;
+        const int key = 32 * kw + 8 * (r >> 2) + 4 * half + (r & 3);  // inside the 64-key tile
 #pragma unroll
-        for (int dt = 0; dt < BDT; ++dt) {
-            pk[32 * dt + col] = dk[dt][r] * scale;
-            pv[32 * dt + col] = dv[dt][r];
-        }
+        for (int dt = 0; dt < BDT; ++dt) dst[key * BD + 32 * dt + col] = acc[dt][r] * osc;
     }
 }
 
@@ -617,7 +616,7 @@ hipError_t launch_bwd_g(const BwdArgs& a, hipStream_t stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.nseg > 0) {
-        hipLaunchKernelGGL((bwd_dkdv_kernel<D, G, BW>), dim3((unsigned)(a.nseg * bhk)), dim3(128), 0,
+        hipLaunchKernelGGL((bwd_dkdv_kernel<D, G, BW>), dim3((unsigned)(a.nseg * bhk)), dim3(256), 0,
                            stream, (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
                            (const __bf16*)a.dO, a.lse2, a.delta, a.dK, a.dV, a.part, a.segs,
                            a.users, a.nslots, (int32_t)a.n, bhk, a.Hkv, c_log2, scale);
