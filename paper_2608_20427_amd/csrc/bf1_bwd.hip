@@ -1,5 +1,5 @@
 // BF1 causal dyadic block-sparse attention: backward kernels for gfx950
-// (head_dim 128).  Gradients of O = softmax_mask(c Q K^T) V with respect to Q,
+// (head_dim 64 and 128).  Gradients of O = softmax_mask(c Q K^T) V with respect to Q,
 // K and V for an upstream gradient dO, on the route of the paper's §3.1
 // (Eq. 1), with P recomputed from the forward's log-sum-exp:
 //     P = exp(c S - LSE),  D = rowsum(dO * O),  dP = dO V^T,  dS = P * (dP - D),
@@ -11,15 +11,15 @@
 //    and LSE log2 e for its rows (written for the next kernel) and dQ.
 //  * bwd_dkdv_kernel -- one workgroup per (batch, kv-head, 64-key tile,
 //    segment of the tile's query-block list), walking the TRANSPOSED route
-//    (the query blocks that select the key block); accumulates dK and dV in
-//    registers.  Key block 0 is selected by every query block, so long lists
+//    (the query blocks that select the key block); two waves accumulate dV
+//    and two dK in registers.  Key block 0 is selected by every query block, so long lists
 //    are cut into segments whose partial sums go to a workspace.
 //  * bwd_reduce_kernel -- sums the segment partials of such tiles in a fixed
 //    order (deterministic) into dK and dV.
 //
 // Tiles in LDS keep the natural [row][d] order in 16-byte chunks; chunk c of
-// row r sits at c ^ bswz(r), bswz(r) = 4 (r mod 4) + (r/4 mod 4).  This one
-// layout is conflict-free for both ways the backward reads a tile: 16 bytes
+// row r sits at c ^ bswz(r) (for d = 128, bswz(r) = 4 (r mod 4) + (r/4 mod 4);
+// d = 64 has its own, below).  This one layout is conflict-free for both ways the backward reads a tile: 16 bytes
 // of one row per lane (an MFMA operand with k along d) and the LDS transpose
 // load (an operand with k along the rows).  Matrix-core layouts follow the
 // forward (v_mfma_f32_32x32x16_bf16; accumulator lane l, register r holds
