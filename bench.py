@@ -244,8 +244,9 @@ def backward_point(torch, bf1, synth, w, q, k, v, warmup, reps):
             "bwd_algorithmic_gflop": flops / 1e9, "bwd_tflops": tf,
             "bwd_pct_peak": 100 * tf / PEAK_BF16_TFLOPS,
             "workspace_mb": ws.numel() / 1e6,
-            "kernels": "Delta+dQ (bwd_dq_kernel), dK/dV (bwd_dkdv_kernel), partial reduce "
-                       "(bwd_reduce_kernel); per-kernel times are in the rocprofv3 summary"}
+            "kernels": "D and LSE log2 e (bwd_delta_kernel), dK/dV and dS (bwd_dkdv_kernel), "
+                       "partial reduce (bwd_reduce_kernel), dQ from dS (bwd_dq_kernel); "
+                       "per-kernel times are in the rocprofv3 summary"}
 
 
 def variants_point(torch, bf1, w, q, k, v, warmup, reps):

@@ -150,10 +150,14 @@ int bf1_plan_transposed(int64_t n, int32_t B, int32_t L,
  *              contents on entry are irrelevant and are clobbered.
  * Supported: head_dim in {64, 128}, B in {64, 128}, G = Hq/Hkv in {1, 2, 4, 8}
  * with G * B >= 128 (so G = 1 needs B = 128); others return BF1_ERR_UNSUPPORTED.
- * Three kernels on `stream`: dQ (also writes D and LSE log2 e to the workspace), dK/dV
- * over the transposed route (cut into segments of at most 16 query blocks;
- * the segments of long lists -- block 0 -- leave partial sums in the
- * workspace), and a fixed-order sum of those partials.  The route and its
+ * Four kernels on `stream`: D and LSE log2 e per query row (to the
+ * workspace); dK/dV over the transposed route (cut into segments of at most
+ * 16 query blocks; the segments of long lists -- block 0 -- leave partial
+ * sums in the workspace), which also writes dS (bf16, one 8 KB unit per
+ * selected block pair, q-head and pair of 64-row sub-tiles) to the workspace;
+ * a fixed-order sum of the partials; and dQ = dS K / sqrt(d) from the stored
+ * dS along the forward route.  The workspace therefore grows with the number
+ * of selected pairs (670 MB at n = 32768 with 16 q-heads, b = 64).  The route and its
  * transpose are cached per (device, n, B, L) like bf1_attn_fwd's.  The result
  * is deterministic.
  */

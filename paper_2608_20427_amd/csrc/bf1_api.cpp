@@ -148,8 +148,9 @@ int get_plan(int64_t n, int32_t B, int32_t L, hipStream_t s, Plan* out) {
 constexpr int64_t SEG_MAX = 16;
 
 struct BwdLayout {
-    std::vector<int32_t> users, segs, reds;
+    std::vector<int32_t> users, uoffs, segs, reds;
     int32_t nslots = 0;
+    int64_t nusers = 0;
 };
 
 bool bwd_layout(int64_t n, int32_t B, int32_t L, BwdLayout* lay, bool fill) {
@@ -161,6 +162,7 @@ bool bwd_layout(int64_t n, int32_t B, int32_t L, BwdLayout* lay, bool fill) {
     for (int64_t i = 0; i < NB; ++i) {
         const int64_t cnt = bf1::route_users(NB, L, i, nullptr);
         const int64_t off = total;
+        if (fill) lay->uoffs.push_back((int32_t)off);
         if (fill) {
             tmp.resize(cnt);
             bf1::route_users(NB, L, i, tmp.data());
@@ -185,6 +187,7 @@ bool bwd_layout(int64_t n, int32_t B, int32_t L, BwdLayout* lay, bool fill) {
         }
     }
     if (fill) {
+        lay->uoffs.push_back((int32_t)total);
         std::stable_sort(segs.begin(), segs.end(),
                          [](const std::array<int32_t, 8>& a, const std::array<int32_t, 8>& b) {
                              return a[3] > b[3];
@@ -192,11 +195,14 @@ bool bwd_layout(int64_t n, int32_t B, int32_t L, BwdLayout* lay, bool fill) {
         for (auto& sg : segs) lay->segs.insert(lay->segs.end(), sg.begin(), sg.end());
     }
     lay->nslots = (int32_t)nslots;
+    lay->nusers = total;
     return true;
 }
 
 struct BwdPlan {
     int32_t* users = nullptr;
+    int32_t* uoffs = nullptr;
+    int64_t nusers = 0;
     int32_t* segs = nullptr;
     int32_t* reds = nullptr;
     int32_t nseg = 0, nred = 0, nslots = 0;
@@ -209,7 +215,9 @@ int bwd_workspace_bytes(int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32
     if (!bwd_layout(n, B, L, &lay, false)) return BF1_ERR_INVALID_ARG;
     const int64_t delta = ((int64_t)batch * Hq * n * 4 + 255) / 256 * 256;
     const int64_t part = (int64_t)batch * Hkv * lay.nslots * 2 * 64 * head_dim * 4;
-    *bytes = 2 * delta + part;  // D, LSE * log2 e, partial tiles
+    const int64_t nsub = B / 64;
+    const int64_t ds = (int64_t)batch * Hq * lay.nusers * nsub * nsub * 64 * 64 * 2;
+    *bytes = 2 * delta + part + ds;  // D, LSE * log2 e, partial tiles, dS units
     return BF1_OK;
 }
 
@@ -226,6 +234,7 @@ int get_bwd_plan(int64_t n, int32_t B, int32_t L, BwdPlan* out) {
         p.nseg = (int32_t)(lay.segs.size() / 8);
         p.nred = (int32_t)(lay.reds.size() / 4);
         p.nslots = lay.nslots;
+        p.nusers = lay.nusers;
         auto up = [](const std::vector<int32_t>& v, int32_t** d) -> bool {
             const size_t bytes = sizeof(int32_t) * (v.empty() ? 1 : v.size());
             if (hipMalloc((void**)d, bytes) != hipSuccess) return false;
@@ -234,8 +243,10 @@ int get_bwd_plan(int64_t n, int32_t B, int32_t L, BwdPlan* out) {
                 return false;
             return true;
         };
-        if (!up(lay.users, &p.users) || !up(lay.segs, &p.segs) || !up(lay.reds, &p.reds)) {
+        if (!up(lay.users, &p.users) || !up(lay.uoffs, &p.uoffs) || !up(lay.segs, &p.segs) ||
+            !up(lay.reds, &p.reds)) {
             (void)hipFree(p.users);
+            (void)hipFree(p.uoffs);
             (void)hipFree(p.segs);
             (void)hipFree(p.reds);
             return BF1_ERR_NOMEM;
@@ -467,9 +478,11 @@ int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, con
     float* delta = (float*)workspace;
     float* lse2 = (float*)((char*)workspace + delta_bytes);
     float* part = (float*)((char*)workspace + 2 * delta_bytes);
-    bf1::BwdArgs a{Q, K, V, O, dO, LSE, dQ, dK, dV, delta, lse2, part,
-                   plan.row_ptr, plan.col_idx, plan.nnz, bp.users, bp.segs, bp.nseg,
-                   bp.reds, bp.nred, bp.nslots, batch, n, Hq, Hkv, B, head_dim};
+    void* ds = (char*)workspace + 2 * delta_bytes +
+               (int64_t)batch * Hkv * bp.nslots * 2 * 64 * head_dim * 4;
+    bf1::BwdArgs a{Q, K, V, O, dO, LSE, dQ, dK, dV, delta, lse2, part, ds,
+                   plan.row_ptr, plan.col_idx, plan.nnz, bp.users, bp.uoffs, bp.nusers, bp.segs, bp.nseg,
+                   bp.reds, bp.nred, bp.nslots, batch, n, Hq, Hkv, B, head_dim, L};
     return status_of(bf1::launch_backward(a, s));
 }
 
@@ -485,6 +498,7 @@ void bf1_release_plans(void) {
     if (!g_bwd_plans.empty()) (void)hipDeviceSynchronize();
     for (auto& kv : g_bwd_plans) {
         (void)hipFree(kv.second.users);
+        (void)hipFree(kv.second.uoffs);
         (void)hipFree(kv.second.segs);
         (void)hipFree(kv.second.reds);
     }

@@ -5,17 +5,19 @@
 //     P = exp(c S - LSE),  D = rowsum(dO * O),  dP = dO V^T,  dS = P * (dP - D),
 //     dQ = c dS K,  dK = c dS^T Q,  dV = P^T dO   (summed over a GQA group).
 //
-// Kernels:
-//  * bwd_dq_kernel   -- one workgroup per (batch, kv-head, query block, row
-//    chunk), walking the forward route like the forward kernel; computes D
-//    and LSE log2 e for its rows (written for the next kernel) and dQ.
+// Kernels, in launch order:
+//  * bwd_delta_kernel -- D and LSE log2 e of every query row.
 //  * bwd_dkdv_kernel -- one workgroup per (batch, kv-head, 64-key tile,
 //    segment of the tile's query-block list), walking the TRANSPOSED route
 //    (the query blocks that select the key block); two waves accumulate dV
-//    and two dK in registers.  Key block 0 is selected by every query block, so long lists
+//    and two dK in registers, and the dS it forms is written to the workspace
+//    for dQ.  Key block 0 is selected by every query block, so long lists
 //    are cut into segments whose partial sums go to a workspace.
 //  * bwd_reduce_kernel -- sums the segment partials of such tiles in a fixed
 //    order (deterministic) into dK and dV.
+//  * bwd_dq_kernel   -- one workgroup per (batch, kv-head, query block, row
+//    chunk), walking the forward route like the forward kernel: dQ from the
+//    stored dS and the K tiles (no score is recomputed).
 //
 // Tiles in LDS keep the natural [row][d] order in 16-byte chunks; chunk c of
 // row r sits at c ^ bswz(r) (for d = 128, bswz(r) = 4 (r mod 4) + (r/4 mod 4);
@@ -30,6 +32,7 @@
 
 #include "bf1_device.h"
 #include "bf1_kernels.h"
+#include "bf1_route.h"
 
 namespace bf1 {
 namespace {
@@ -81,32 +84,74 @@ __device__ __forceinline__ float dot_bf16x8(u32x4 a, u32x4 b) {
 }
 
 // ---------------------------------------------------------------------------
-// dQ (and D)
+// dS units
 // ---------------------------------------------------------------------------
-// Workgroup = 4 waves x 32 stacked query rows (like the forward); per tile of
-// 64 keys each wave computes S^T = K Q^T and dP^T = V dO^T (A operands: rows
-// of the K and V tiles; B operands: this lane's query row of Q and dO, held in
-// registers), P^T = exp2(c log2e S^T - log2e LSE), dS^T = P^T (dP^T - D), and
-// dQ^T += K^T dS^T (A operand: transpose reads of the K tile; B: dS^T packed
-// to bf16 from the lane's own registers).  Double-buffered K/V tiles, one
-// barrier per tile.
-template <int D, int G, int BW, bool DENSE>
-__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
-    const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
-    const __bf16* __restrict__ O, const __bf16* __restrict__ dO, const float* __restrict__ LSE,
-    float* __restrict__ dQ, float* __restrict__ Delta, float* __restrict__ Lse2,
-    const int32_t* __restrict__ row_ptr,
-    const int32_t* __restrict__ col_idx, int64_t nnz, int32_t n, int32_t NB, int32_t batch_hkv,
-    int32_t Hkv, float c_log2, float scale) {
+// The dK/dV kernel forms dS = P (dP - D) of every selected (64-row query tile,
+// 64-key tile, q-head) and writes it, bf16, to the workspace for the dQ
+// kernel: one 8 KB unit per triple, unit index
+//   (((batch x kv-head, transposed-route entry), query sub-tile), key sub-tile), head in group.
+// A unit is stored in the dQ kernel's MFMA operand order: 16-byte piece
+// (rh, t, lane) at ((4 rh + t) 64 + lane) 16 holds, for query 32 rh + lane % 32,
+// the keys 16 t + 4 h + {0..3} and 16 t + 8 + 4 h + {0..3} (h = lane / 32):
+// the B operand of k-step t of dQ^T += K^T dS^T, loaded straight into registers.
+constexpr int DS_UNIT = KT * KT * 2;  // bytes per unit
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
+
+// ---------------------------------------------------------------------------
+// D and LSE log2 e
+// ---------------------------------------------------------------------------
+// D = rowsum(dO * O) of every query row (fp32, summed over the row's D / 8
+// lanes by butterfly shuffles) and LSE * log2 e beside it, for the dK/dV
+// kernel.  One lane per 16 bytes of a row.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict__ O, const __bf16* __restrict__ dO,
+                                                        const float* __restrict__ LSE, float* __restrict__ Delta,
+                                                        float* __restrict__ Lse2, int64_t rows) {
+    constexpr int LPR = D / 8;  // lanes per row
+    constexpr int RPB = 256 / LPR;
+    const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
+    const int c = threadIdx.x % LPR;
+    float s = 0.f;
+    if (row < rows) {
+        const u32x4 wo = reinterpret_cast<const u32x4*>(O + row * D)[c];
+        const u32x4 wd = reinterpret_cast<const u32x4*>(dO + row * D)[c];
+        s = dot_bf16x8(wd, wo);
+    }
+#pragma unroll
+    for (int m = LPR / 2; m > 0; m >>= 1) s += __shfl_xor(s, m);
+    if (row < rows && c == 0) {
+        Delta[row] = s;
+        Lse2[row] = LSE[row] * LOG2E;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// dQ
+// ---------------------------------------------------------------------------
+// Workgroup = 4 waves x 32 stacked query rows (like the forward), walking the
+// forward route.  dS comes from the dK/dV kernel's units, so nothing is
+// recomputed: per 64-key tile the workgroup stages the K tile in LDS
+// (buffer->LDS DMA, double-buffered, one barrier per tile), each wave loads
+// its rows' dS^T operands from the unit straight into registers, and
+// accumulates dQ^T += K^T dS^T (A: transpose reads of the K tile).  Both loads
+// of tile k+1 are issued before the MFMAs of tile k.  32 KB of LDS and ~120
+// registers give four workgroups per CU, which together keep enough loads in
+// flight to cover the HBM latency of the dS units (each is read once).
+template <int D, int G, int BW>
+__global__ __launch_bounds__(256, 4) void bwd_dq_kernel(
+    const __bf16* __restrict__ K, const __bf16* __restrict__ dS, float* __restrict__ dQ,
+    const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t nnz,
+    const int32_t* __restrict__ uoffs, int64_t nusers, int32_t n, int32_t NB, int32_t L,
+    int32_t batch_hkv, int32_t Hkv, float scale) {
     BWD_GEOMETRY(D);
     constexpr int NW = 4, ROWS = 128;
     constexpr int NCHUNK = (G * BW) / ROWS;
     constexpr int NSUB = BW / KT;
-    constexpr int SPW = (BTILE / 1024) / NW;  // K (or V) segments per wave per tile
+    constexpr int SPW = (BTILE / 1024) / NW;  // K segments per wave per tile
     static_assert(NCHUNK * ROWS == G * BW, "rows must tile the stacked group");
-
-    __shared__ u32x4 kt_s[2][BTILE / 16];
-    __shared__ u32x4 vt_s[2][BTILE / 16];
+    // K tiles (two buffers); the epilogue reuses the space as four 8 KB slices
+    constexpr int LDS_BYTES = 2 * BTILE > 32768 ? 2 * BTILE : 32768;
+    __shared__ u32x4 lds[LDS_BYTES / 16];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -127,52 +172,22 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
     const int head = g * G + srow / BW;
     const int qin = srow % BW + col;  // query position inside block j
     const int32_t qpos = j * BW + qin;
-    const bool qvalid = qpos < n;
     const int64_t qrow = ((int64_t)beta * Hq + head) * (int64_t)n + qpos;
-
-    // ---- Q, dO rows (B operands) and D = dO . O --------------------------------
-    bf16x8 qf[BKS], dof[BKS];
-    float dpart = 0.f;
-    {
-        const u32x4* qs = reinterpret_cast<const u32x4*>(Q + qrow * BD);
-        const u32x4* ds = reinterpret_cast<const u32x4*>(dO + qrow * BD);
-        const u32x4* os = reinterpret_cast<const u32x4*>(O + qrow * BD);
-#pragma unroll
-        for (int s = 0; s < BKS; ++s) {
-            u32x4 wq = {0u, 0u, 0u, 0u}, wd = wq, wo = wq;
-            if (qvalid) {
-                wq = qs[2 * s + half];
-                wd = ds[2 * s + half];
-                wo = os[2 * s + half];
-            }
-            qf[s] = __builtin_bit_cast(bf16x8, wq);
-            dof[s] = __builtin_bit_cast(bf16x8, wd);
-            dpart += dot_bf16x8(wd, wo);
-        }
-    }
-    const float Dq = pair_sum(dpart);  // the two lane halves hold the two halves of d
-    const float lse2 = qvalid ? LSE[qrow] * LOG2E : INFINITY;  // rows past n: P = 0
-    if (qvalid && half == 0) {  // D and LSE log2 e of the row, for the dK/dV kernel
-        Delta[qrow] = Dq;
-        Lse2[qrow] = lse2;
-    }
+    // dS unit of this wave's rows: head in the group, query sub-tile; the
+    // wave's 32 rows are half rh_w of the unit
+    const int rh_w = (srow % KT) / 32;
+    const int u_hh = srow / BW, u_qs = (srow % BW) / KT;
 
     // ---- route walk (as in the forward) -------------------------------------------
-    int32_t pos_end, cur_p;
-    if (DENSE) {
-        cur_p = 0;
-        pos_end = j + 1;
-    } else {
-        int64_t e0 = row_ptr[j], e1 = row_ptr[j + 1];
-        e0 = e0 < 0 ? 0 : (e0 > nnz ? nnz : e0);
-        e1 = e1 < e0 ? e0 : (e1 > nnz ? nnz : e1);
-        cur_p = (int32_t)e0;
-        pos_end = (int32_t)e1;
-    }
+    int64_t e0 = row_ptr[j], e1 = row_ptr[j + 1];
+    e0 = e0 < 0 ? 0 : (e0 > nnz ? nnz : e0);
+    e1 = e1 < e0 ? e0 : (e1 > nnz ? nnz : e1);
+    int32_t cur_p = (int32_t)e0;
+    const int32_t pos_end = (int32_t)e1;
     int cur_u = 0;
     auto next_tile = [&](int32_t& ti, int& tu) -> bool {
         while (cur_p < pos_end) {
-            const int32_t i = DENSE ? cur_p : col_idx[cur_p];
+            const int32_t i = col_idx[cur_p];
             if (i >= 0 && i <= j) {
                 for (; cur_u < NSUB; ++cur_u)
                     if (i * BW + cur_u * KT < n) {
@@ -191,18 +206,21 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
         return false;
     };
 
-    const uint32_t head_bytes = (uint32_t)n * BRB;
     const __amdgpu_buffer_rsrc_t k_rsrc =
-        head_rsrc(K + ((int64_t)beta * Hkv + g) * (int64_t)n * BD, head_bytes);
-    const __amdgpu_buffer_rsrc_t v_rsrc =
-        head_rsrc(V + ((int64_t)beta * Hkv + g) * (int64_t)n * BD, head_bytes);
-    auto stage = [&](int buf, int32_t ti, int tu) {
-        const uint32_t soff = (uint32_t)(ti * BW + tu * KT) * BRB;
+        head_rsrc(K + ((int64_t)beta * Hkv + g) * (int64_t)n * BD, (uint32_t)n * BRB);
+    // dS operands of tile (ti, tu) into registers, then its K tile into LDS
+    auto stage = [&](int buf, int32_t ti, int tu, u32x4 (&dsr)[4]) {
+        const int32_t tiu = __builtin_amdgcn_readfirstlane(ti), tuu = __builtin_amdgcn_readfirstlane(tu);
+        const int64_t et = (int64_t)__builtin_amdgcn_readfirstlane(uoffs[tiu]) + route_user_rank(L, tiu, j);
+        const int64_t ui = ((((int64_t)bh * nusers + et) * NSUB + u_qs) * NSUB + tuu) * G + u_hh;
+        const u32x4* src = reinterpret_cast<const u32x4*>(dS + ui * (DS_UNIT / 2)) + 4 * 64 * rh_w + lane;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) dsr[t] = __builtin_nontemporal_load(src + 64 * t);
+        const uint32_t soff = (uint32_t)(tiu * BW + tuu * KT) * BRB;
 #pragma unroll
         for (int it = 0; it < SPW; ++it) {
             const int seg = it * NW + wave;
-            load_lds_async<16>(k_rsrc, &kt_s[buf][seg * 64], seg_off<D>(seg, lane), soff);
-            load_lds_async<16>(v_rsrc, &vt_s[buf][seg * 64], seg_off<D>(seg, lane), soff);
+            load_lds_async<16>(k_rsrc, &lds[buf * (BTILE / 16) + seg * 64], seg_off<D>(seg, lane), soff);
         }
     };
 
@@ -214,68 +232,32 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
 
     int32_t ti = 0, tn = 0;
     int tu = 0, tnu = 0;
+    u32x4 dcur[4], dnext[4];
     bool have = next_tile(ti, tu);
-    if (have) stage(0, ti, tu);
+    if (have) stage(0, ti, tu, dcur);
     __builtin_amdgcn_s_waitcnt(VMCNT0);
     __syncthreads();
     int buf = 0;
-    const f32x16 zero = {};
     while (have) {
         const bool hn = next_tile(tn, tnu);
-        if (hn) stage(buf ^ 1, tn, tnu);
+        if (hn) stage(buf ^ 1, tn, tnu, dnext);
 
-        const char* kb = reinterpret_cast<const char*>(&kt_s[buf][0]);
-        const char* vb = reinterpret_cast<const char*>(&vt_s[buf][0]);
-        f32x16 st[2], dpt[2];
+        const uint32_t kl = lds_addr(&lds[0]) + buf * BTILE;
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
+        for (int t = 0; t < 4; ++t) {
+            const bf16x8 db = __builtin_bit_cast(bf16x8, dcur[t]);
 #pragma unroll
-            for (int ks = 0; ks < BKS; ++ks) {
-                const int o = rw_off<D>(32 * kt + col, 2 * ks + half);
-                const u32x4 ka = *reinterpret_cast<const u32x4*>(kb + o);
-                const u32x4 va = *reinterpret_cast<const u32x4*>(vb + o);
-                st[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    __builtin_bit_cast(bf16x8, ka), qf[ks], ks == 0 ? zero : st[kt], 0, 0, 0);
-                dpt[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    __builtin_bit_cast(bf16x8, va), dof[ks], ks == 0 ? zero : dpt[kt], 0, 0, 0);
-            }
-        // dS^T = P^T (dP^T - D), packed as the B operands of K^T dS^T
-        bf16x8 db[4];
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) st[kt][r] = __builtin_amdgcn_exp2f(fmaf(st[kt][r], c_log2, -lse2));
-        if (ti == j) {  // the key-block-diagonal tile: token-level causal mask
-#pragma unroll
-            for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (tu * KT + 32 * kt + 8 * (r >> 2) + 4 * half + (r & 3) > qin) st[kt][r] = 0.f;
-        }
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-            f32x8 v8;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                v8[r & 7] = st[kt][r] * (dpt[kt][r] - Dq);
-                if ((r & 7) == 7) db[2 * kt + (r >> 3)] = __builtin_convertvector(v8, bf16x8);
-            }
-        }
-        const uint32_t kl = lds_addr(kb);
-#pragma unroll
-        for (int dt = 0; dt < BDT; ++dt) {
-            const uint32_t a0 = kl + tr_off<D>(lane, dt, 0), a1 = kl + tr_off<D>(lane, dt, 1);
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const u32x2 lo = lds_read_tr16(a0 + 16 * t * BRB);
-                const u32x2 hi = lds_read_tr16(a1 + 16 * t * BRB);
-                const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
-                acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w),
-                                                                  db[t], acc[dt], 0, 0, 0);
+            for (int dt = 0; dt < BDT; ++dt) {
+                const u32x2 alo = lds_read_tr16(kl + tr_off<D>(lane, dt, 0) + 16 * t * BRB);
+                const u32x2 ahi = lds_read_tr16(kl + tr_off<D>(lane, dt, 1) + 16 * t * BRB);
+                const u32x4 w = {alo[0], alo[1], ahi[0], ahi[1]};
+                acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w), db, acc[dt], 0, 0, 0);
             }
         }
         __builtin_amdgcn_s_waitcnt(VMCNT0);  // this wave's loads of the next tile have landed
         __syncthreads();                      // ... and every other wave's; this tile is free
+#pragma unroll
+        for (int t = 0; t < 4; ++t) dcur[t] = dnext[t];
         ti = tn;
         tu = tnu;
         have = hn;
@@ -283,31 +265,32 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
     }
     __builtin_amdgcn_s_waitcnt(VMCNT0);
 
-    // ---- dQ = c dS K, staged through LDS into whole-row stores (rows past n skipped) ----
+    // ---- dQ = c dS K, staged through an 8 KB LDS slice per wave, 64 columns at a
+    // time, into half-row (256-byte) stores; rows past n skipped ----
     {
-        constexpr int QCH = BD / 4;  // 16-byte chunks per fp32 row
-        char* slice = wave == 0 ? reinterpret_cast<char*>(&kt_s[0][0])
-                    : wave == 1 ? reinterpret_cast<char*>(&kt_s[1][0])
-                    : wave == 2 ? reinterpret_cast<char*>(&vt_s[0][0])
-                                : reinterpret_cast<char*>(&vt_s[1][0]);
+        char* slice = reinterpret_cast<char*>(&lds[0]) + wave * 8192;
+        const int64_t row0 = qrow - col;  // first row of this wave
 #pragma unroll
-        for (int dt = 0; dt < BDT; ++dt)
+        for (int rd = 0; rd < BDT / 2; ++rd) {
 #pragma unroll
-            for (int gq4 = 0; gq4 < 4; ++gq4) {
-                f32x4 v4;
+            for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
-                for (int c = 0; c < 4; ++c) v4[c] = acc[dt][4 * gq4 + c] * scale;
-                const int ch = (8 * dt + 2 * gq4 + half) ^ (col & 15);
-                *reinterpret_cast<f32x4*>(slice + col * (BD * 4) + ch * 16) = v4;
+                for (int gq4 = 0; gq4 < 4; ++gq4) {
+                    f32x4 v4;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) v4[c] = acc[2 * rd + dd][4 * gq4 + c] * scale;
+                    const int ch = (8 * dd + 2 * gq4 + half) ^ (col & 15);
+                    *reinterpret_cast<f32x4*>(slice + col * 256 + ch * 16) = v4;
+                }
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): these 64 columns are in LDS
+#pragma unroll
+            for (int it = 0; it < 8; ++it) {
+                const int r = it * 4 + lane / 16, c = lane % 16;
+                const f32x4 w = *reinterpret_cast<const f32x4*>(slice + r * 256 + ((c ^ (r & 15)) * 16));
+                if (qpos - col + r < n)
+                    __builtin_nontemporal_store(w, reinterpret_cast<f32x4*>(dQ + (row0 + r) * BD + 64 * rd + c * 4));
             }
-        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's dQ tile is in LDS
-        const int64_t row0 = qrow - col;      // first row of this wave
-        constexpr int RPI = 64 / QCH;         // rows per store instruction
-#pragma unroll
-        for (int it = 0; it < 32 / RPI; ++it) {
-            const int r = it * RPI + lane / QCH, c = lane % QCH;
-            const f32x4 w = *reinterpret_cast<const f32x4*>(slice + r * (BD * 4) + ((c ^ (r & 15)) * 16));
-            if (qpos - col + r < n) __builtin_nontemporal_store(w, reinterpret_cast<f32x4*>(dQ + (row0 + r) * BD + c * 4));
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // read back before the next columns overwrite it
         }
     }
 }
@@ -326,6 +309,9 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
 //   phase 2: dS waves read P; dS = P (dP - D)                (lane = key column)
 //   phase 3: dV += P^T dO (P waves) or dK += dS^T Q (dS waves)
 //            (A: P / dS packed from the lane's own registers; B: transpose reads)
+// The dS waves also write each half's dS (bf16, the values their dK MFMAs
+// use) to the tile's dS unit, transposed through a 2 KB LDS scratch per wave
+// into the dQ kernel's operand order.
 // Splitting the roles halves each wave's registers (no accumulator leaves the
 // VGPRs) and gives two workgroups, two waves per SIMD, per CU.  Two barriers
 // per half order the exchange of P.  A segment descriptor (int32 x 8): key
@@ -335,8 +321,8 @@ template <int D, int G, int BW>
 __global__ __launch_bounds__(256, 2) void bwd_dkdv_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     const __bf16* __restrict__ dO, const float* __restrict__ Lse2, const float* __restrict__ Delta,
-    float* __restrict__ dK, float* __restrict__ dV, float* __restrict__ part,
-    const int32_t* __restrict__ segs, const int32_t* __restrict__ users, int32_t nslots,
+    float* __restrict__ dK, float* __restrict__ dV, float* __restrict__ part, __bf16* __restrict__ dSw,
+    const int32_t* __restrict__ segs, const int32_t* __restrict__ users, int32_t nslots, int64_t nusers,
     int32_t n, int32_t batch_hkv, int32_t Hkv, float c_log2, float scale) {
     BWD_GEOMETRY(D);
     constexpr int NW = 4;
@@ -349,6 +335,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv_kernel(
     __shared__ float lse_s[2][KT];
     __shared__ float del_s[2][KT];
     __shared__ f32x4 p_x[2][4][64];  // P of the current half: [key half][row group][lane]
+    __shared__ u32x2 dsx[2][32 * 8];  // dS transpose scratch of the dS waves: [key half][key][8-byte chunk]
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -371,6 +358,21 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv_kernel(
     const int Hq = Hkv * G;
 
     const int kin = u * KT + 32 * kw + col;  // key position inside block i of this lane's column
+    // transpose-read offsets in the dS scratch: for 16-key step tp, lane (gq, l16)
+    // reads the 8-byte run of queries 16 (gq & 1) + 4 (l16 & 3) of key
+    // 16 tp + 4 (gq >> 1) + l16 / 4 (+8 for the second read)
+    int xoff[2][2];
+    {
+        const int gq = lane >> 4, l16 = lane & 15;
+        const int c8 = 4 * (gq & 1) + (l16 & 3);
+#pragma unroll
+        for (int tp = 0; tp < 2; ++tp)
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const int key = 16 * tp + 4 * (gq >> 1) + (l16 >> 2) + 8 * h2;
+                xoff[tp][h2] = key * 64 + ((c8 ^ (key >> 2)) & 7) * 8;
+            }
+    }
     const int32_t kpos = i * BW + kin;
     const int64_t kvrow0 = ((int64_t)beta * Hkv + g) * (int64_t)n;
 
@@ -427,6 +429,10 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv_kernel(
         const int32_t jq = tile_query_block(t);
         const bool self = jq == i;
         const int qsub = (t % NSUB) * KT;  // query position of tile row 0 inside block jq
+        // this tile's dS unit (dS waves write it for the dQ kernel)
+        char* dsu = reinterpret_cast<char*>(dSw) +
+                    (((((int64_t)bh * nusers + uoff + t / (G * NSUB)) * NSUB + t % NSUB) * NSUB + u) * G +
+                     (t / NSUB) % G) * DS_UNIT;
         // phase-1 rows (Q for S, dO for dP); phase-3 transposed tile (dO for dV, Q for dK)
         const char* ab = reinterpret_cast<const char*>(pw ? &q_s[buf][0] : &o_s[buf][0]);
         const uint32_t tl = lds_addr(pw ? &o_s[buf][0] : &q_s[buf][0]);
@@ -487,6 +493,28 @@ __global__ __launch_bounds__(256, 2) void bwd_dkdv_kernel(
                         const int r = 4 * g4 + c;
                         pk2[r >> 3][r & 7] = (__bf16)(pp[g4][c] * (sc[r] - rv[g4][c]));
                     }
+                // dS of this half to the workspace in the dQ kernel's operand order:
+                // transposed (key rows -> query lanes) through the wave's 2 KB
+                // scratch, 8-byte chunk c8 of row k at c8 ^ (k / 4) (conflict-free)
+                const uint32_t xb = lds_addr(&dsx[0][0]) + kw * 2048;
+#pragma unroll
+                for (int m = 0; m < 2; ++m) {
+                    const u32x4 w = __builtin_bit_cast(u32x4, pk2[m]);
+#pragma unroll
+                    for (int sec = 0; sec < 2; ++sec) {
+                        const int c8 = 4 * m + 2 * sec + half;  // queries 16 m + 8 sec + 4 half + 0..3
+                        *reinterpret_cast<lds_u32x2*>(static_cast<uintptr_t>(xb + col * 64 + ((c8 ^ (col >> 2)) & 7) * 8)) =
+                            u32x2{w[2 * sec], w[2 * sec + 1]};
+                    }
+                }
+                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+#pragma unroll
+                for (int tp = 0; tp < 2; ++tp) {
+                    const u32x2 lo = lds_read_tr16(xb + xoff[tp][0]);
+                    const u32x2 hi = lds_read_tr16(xb + xoff[tp][1]);
+                    __builtin_nontemporal_store(u32x4{lo[0], lo[1], hi[0], hi[1]},
+                                                reinterpret_cast<u32x4*>(dsu + ((4 * rh + 2 * kw + tp) * 64 + lane) * 16));
+                }
             }
             // ---- phase 3: transpose reads of dO (P waves) or Q (dS waves), as one group
             u32x4 wt[BDT][2];
@@ -605,21 +633,23 @@ hipError_t launch_bwd_g(const BwdArgs& a, hipStream_t stream) {
     const int32_t NB = (int32_t)((a.n + BW - 1) / BW);
     const int32_t bhk = a.batch * a.Hkv;
     const int64_t items = (int64_t)NB * bhk * NCHUNK;
-    if (items > 0x7fffffff || (int64_t)a.nseg * bhk > 0x7fffffff || (int64_t)a.nred * bhk > 0x7fffffff)
+    const int64_t rows = (int64_t)a.batch * a.Hq * a.n;
+    const int64_t dgrid = (rows + 256 / (D / 8) - 1) / (256 / (D / 8));
+    if (items > 0x7fffffff || dgrid > 0x7fffffff || (int64_t)a.nseg * bhk > 0x7fffffff ||
+        (int64_t)a.nred * bhk > 0x7fffffff)
         return hipErrorInvalidValue;
     const float scale = 1.0f / sqrtf((float)BD);
     const float c_log2 = scale * LOG2E;
-    hipLaunchKernelGGL((bwd_dq_kernel<D, G, BW, false>), dim3((unsigned)items), dim3(256), 0, stream,
-                       (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V, (const __bf16*)a.O,
-                       (const __bf16*)a.dO, a.LSE, a.dQ, a.delta, a.lse2, a.row_ptr, a.col_idx, a.nnz,
-                       (int32_t)a.n, NB, bhk, a.Hkv, c_log2, scale);
+    // D and LSE log2 e, then dK/dV (which also writes dS), the partial sums, dQ
+    hipLaunchKernelGGL((bwd_delta_kernel<D>), dim3((unsigned)dgrid), dim3(256), 0, stream,
+                       (const __bf16*)a.O, (const __bf16*)a.dO, a.LSE, a.delta, a.lse2, rows);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (a.nseg > 0) {
         hipLaunchKernelGGL((bwd_dkdv_kernel<D, G, BW>), dim3((unsigned)(a.nseg * bhk)), dim3(256), 0,
                            stream, (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
-                           (const __bf16*)a.dO, a.lse2, a.delta, a.dK, a.dV, a.part, a.segs,
-                           a.users, a.nslots, (int32_t)a.n, bhk, a.Hkv, c_log2, scale);
+                           (const __bf16*)a.dO, a.lse2, a.delta, a.dK, a.dV, a.part, (__bf16*)a.ds,
+                           a.segs, a.users, a.nslots, a.nusers, (int32_t)a.n, bhk, a.Hkv, c_log2, scale);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -629,8 +659,12 @@ hipError_t launch_bwd_g(const BwdArgs& a, hipStream_t stream) {
         hipLaunchKernelGGL((bwd_reduce_kernel<D, BW>), dim3((unsigned)grid), dim3(256), 0,
                            stream, a.dK, a.dV, a.part, a.reds, a.nslots, (int32_t)a.n, bhk);
         e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    return e;
+    hipLaunchKernelGGL((bwd_dq_kernel<D, G, BW>), dim3((unsigned)items), dim3(256), 0, stream,
+                       (const __bf16*)a.K, (const __bf16*)a.ds, a.dQ, a.row_ptr, a.col_idx, a.nnz,
+                       a.uoffs, a.nusers, (int32_t)a.n, NB, a.L, bhk, a.Hkv, scale);
+    return hipGetLastError();
 }
 
 template <int D, int BW>

@@ -38,10 +38,13 @@ struct BwdArgs {
     float* delta;            // workspace: [batch, Hq, n] fp32 (D = rowsum(dO * O))
     float* lse2;             // workspace: [batch, Hq, n] fp32 (LSE * log2 e)
     float* part;             // workspace: [batch * Hkv, nslots, 2, 64, head_dim] fp32
+    void* ds;                // workspace: dS units, [batch * Hkv, nusers, B/64, B/64, Hq/Hkv] x 8 KB bf16
     const int32_t* row_ptr;  // forward route (CSR)
     const int32_t* col_idx;
     int64_t nnz;
     const int32_t* users;    // transposed route entries (query blocks per key block)
+    const int32_t* uoffs;    // [NB + 1]: first entry of each key block's list in users
+    int64_t nusers;          // entries of the transposed route
     const int32_t* segs;     // [nseg][8]: key block, sub-tile, first entry, count, slot
     int32_t nseg;
     const int32_t* reds;     // [nred][4]: key block, sub-tile, first slot, slot count
@@ -53,6 +56,7 @@ struct BwdArgs {
     int32_t Hkv;
     int32_t B;               // block width 64 or 128
     int32_t head_dim;        // 64 or 128
+    int32_t L;               // local width of the route
 };
 
 hipError_t launch_backward(const BwdArgs& a, hipStream_t stream);

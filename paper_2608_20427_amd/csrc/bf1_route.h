@@ -101,6 +101,17 @@ inline int64_t route_users(int64_t NB, int64_t L, int64_t i, int32_t* out) {
     return c;
 }
 
+// Position of query block j in the list route_users writes for key block i,
+// for a pair (j selects i) of the route: block 0's list is every query block
+// in order; any other list is i itself, its locals at distances 1..L, then the
+// dyadic users at distances 2^r > L in increasing r.  Entries before j are all
+// below j, so the clipping to [0, NB) never changes the position.
+BF1_HD int64_t route_user_rank(int64_t L, int64_t i, int64_t j) {
+    if (i == 0) return j;
+    const int64_t d = j - i;
+    return d <= L ? d : L + 1 + dyadic_count_below(d, L);
+}
+
 // ---- Route variants at BF1's selected-pair budget (§4.3, §5.1, Table 1) ----
 // Both keep |P(j)| blocks in every row, so every query token sees exactly as
 // many keys as under Eq. 1 and the totals (pairs, CSR size) are BF1's.

@@ -124,22 +124,35 @@ def test_plan_transposed_matches_oracle(lib, n, B, L):
     assert ci.tolist() == ci_o.tolist()
 
 
+def _ds_bytes(batch, n, Hq, B, L):
+    # one 64 x 64 bf16 dS unit per (selected block pair, q-head, query and key
+    # sub-tile of 64); the pairs are the entries of the transposed route
+    _, ci = orc.csr_transposed(n, B, L)
+    return batch * Hq * len(ci) * (B // 64) ** 2 * 64 * 64 * 2
+
+
 def test_bwd_workspace_size_head_dim_64(lib):
     # partial dK/dV slots are 64 x head_dim fp32 tiles
     D = (1 * 16 * 32768 * 4 + 255) // 256 * 256
-    assert bf1.bwd_workspace_size(1, 32768, 16, 8, 64, 64, 2) == 2 * D + 1 * 8 * 32 * 2 * 64 * 64 * 4
+    assert bf1.bwd_workspace_size(1, 32768, 16, 8, 64, 64, 2) == (
+        2 * D + 1 * 8 * 32 * 2 * 64 * 64 * 4 + _ds_bytes(1, 32768, 16, 64, 2))
 
 
 def test_bwd_workspace_size(lib):
-    # D and LSE log2 e (each batch * Hq * n fp32, 256-byte rounded) plus the
+    # D and LSE log2 e (each batch * Hq * n fp32, 256-byte rounded), the
     # partial dK/dV slots of the tiles whose query-block list is longer than
-    # one segment of 16: at 32K / b = 64 only block 0 (512 users -> 32
-    # segments).
+    # one segment of 16 (at 32K / b = 64 only block 0: 512 users -> 32
+    # segments), and the dS units.
     D = (1 * 16 * 32768 * 4 + 255) // 256 * 256
     part = 1 * 8 * 32 * 2 * 64 * 128 * 4
-    assert bf1.bwd_workspace_size(1, 32768, 16, 8, 128, 64, 2) == 2 * D + part
+    assert bf1.bwd_workspace_size(1, 32768, 16, 8, 128, 64, 2) == 2 * D + part + _ds_bytes(1, 32768, 16, 64, 2)
     # a short sequence has no split lists
-    assert bf1.bwd_workspace_size(1, 512, 2, 1, 128, 64, 1) == 2 * ((2 * 512 * 4 + 255) // 256 * 256)
+    assert bf1.bwd_workspace_size(1, 512, 2, 1, 128, 64, 1) == (
+        2 * ((2 * 512 * 4 + 255) // 256 * 256) + _ds_bytes(1, 512, 2, 64, 1))
+    # b = 128: four 64 x 64 units per pair and head; block 0's 32 users make two
+    # segments for each of its two 64-key sub-tiles (four partial slots)
+    assert bf1.bwd_workspace_size(2, 4096, 4, 2, 128, 128, 2) == (
+        2 * ((2 * 4 * 4096 * 4 + 255) // 256 * 256) + 2 * 2 * 4 * 2 * 64 * 128 * 4 + _ds_bytes(2, 4096, 4, 128, 2))
 
 
 def test_backward_invalid_arguments_rejected_without_device(lib):
