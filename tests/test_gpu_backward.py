@@ -93,6 +93,8 @@ SMALL = [
     (1, 640, 8, 1, 64, 2),       # G = 8
     (1, 900, 2, 2, 128, 2),      # G = 1 with B = 128
     (1, 1500, 4, 2, 128, 2),     # B = 128, ragged
+    (2, 1300, 8, 2, 128, 2),     # G = 4 with B = 128 (four 128-row chunks per block), batch 2
+    (1, 700, 8, 1, 128, 3),      # G = 8 with B = 128, L = 3
     (1, 2048, 16, 8, 64, 2),     # Qwen geometry, short
     (1, 1, 2, 1, 64, 2),         # a single token
     (1, 65, 2, 1, 64, 2),        # n = B + 1
