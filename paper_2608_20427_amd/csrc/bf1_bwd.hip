@@ -113,8 +113,9 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const __bf16* __restrict
     const int c = threadIdx.x % LPR;
     float s = 0.f;
     if (row < rows) {
-        const u32x4 wo = reinterpret_cast<const u32x4*>(O + row * D)[c];
-        const u32x4 wd = reinterpret_cast<const u32x4*>(dO + row * D)[c];
+        // read once here (the dK/dV kernel re-reads dO tiles much later)
+        const u32x4 wo = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(O + row * D) + c);
+        const u32x4 wd = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(dO + row * D) + c);
         s = dot_bf16x8(wd, wo);
     }
 #pragma unroll
