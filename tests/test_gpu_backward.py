@@ -273,3 +273,27 @@ def test_backward_full_size_peaked_sampled():
     check_bound(dq, ref[0], terms[0], rows=_rows(qb, w.b, w.n), tag="30001 dQ")
     check_bound(dk, ref[1], terms[1], rows=_rows(kv, w.b, w.n), tag="30001 dK")
     check_bound(dv, ref[2], terms[2], rows=_rows(kv, w.b, w.n), tag="30001 dV")
+
+
+@pytest.mark.parametrize("cfg", [(2, 1000, 4, 2, 64, 2), (2, 1300, 8, 2, 128, 2), (1, 777, 4, 1, 64, 3)],
+                         ids=lambda c: "x".join(map(str, c)))
+def test_backward_ignores_workspace_contents(cfg):
+    # Every workspace byte a kernel reads is written earlier in the same call
+    # (D, LSE log2 e, the partial tiles and the dS units of every pair the dQ
+    # kernel visits): a workspace filled with NaN bit patterns gives bitwise
+    # the result of a zeroed one.
+    batch, n, Hq, Hkv, B, L = cfg
+    say(f"backward workspace contents {cfg}")
+    w = synth.Workload("bwd_ws", batch, n, Hq, Hkv, 128, B, L, seed=1234 + n)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    do = synth.make_grad_out(w, device="cuda")
+    o, lse = bf1.attn_fwd(q, k, v, B, L)
+    need = bf1.bwd_workspace_size(batch, n, Hq, Hkv, 128, B, L)
+    outs = []
+    for fill in (0x00, 0xFF):
+        ws = torch.full((need,), fill, dtype=torch.uint8, device="cuda")
+        outs.append(bf1.attn_bwd(q, k, v, o, do, lse, B, L, workspace=ws))
+    torch.cuda.synchronize()
+    for a, b in zip(*outs):
+        assert torch.isfinite(a).all()
+        assert torch.equal(a, b)
