@@ -312,3 +312,23 @@ def test_decode_step_replays_in_a_graph():
         junk = torch.randn(1 << 20, device="cuda").sum()    # eager work between replays
         torch.cuda.synchronize()
         assert torch.isfinite(junk)
+
+
+def test_decode_ignores_workspace_contents():
+    # The merge reads only the records its split kernel wrote in the same call:
+    # a workspace filled with NaN bit patterns gives bitwise the result of a
+    # zeroed one (batch 40: several pages per split, so the merge runs).
+    batch, Hq, Hkv, d, B, L, lens = SPLIT[0]
+    w = synth.DecodeWorkload("dec", batch, max(lens), Hq, Hkv, d, B, L, seed=811)
+    say("decode workspace contents")
+    _, dev = setup_case(w, np.array(lens, dtype=np.int32))
+    plan = bf1.decode_plan(dev["sl"], dev["table"], dev["num_pages"], dev["stride"], w.b, w.L)
+    need = bf1.decode_workspace_size(w.batch, w.Hq, w.Hkv, w.d, dev["stride"])
+    outs = []
+    for fill in (0x00, 0xFF):
+        ws = torch.full((need,), fill, dtype=torch.uint8, device="cuda")
+        outs.append(bf1.attn_decode(dev["q"], dev["kp"], dev["vp"], dev["sl"], plan, w.b, workspace=ws))
+    torch.cuda.synchronize()
+    for a, b in zip(*outs):
+        assert torch.isfinite(a.float()).all()
+        assert torch.equal(a, b)
