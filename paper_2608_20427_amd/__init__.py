@@ -130,6 +130,49 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def check_buffer(t, name, shape, dtype, device):
+    """Raise ValueError unless `t` is a contiguous tensor of exactly `shape`
+    and `dtype` on `device`.  Every buffer handed to the library goes through
+    this check before its pointer is taken: a host tensor, or one of another
+    size, would otherwise become a kernel access outside the intended memory."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a tensor, got {type(t).__name__}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on device {device}, got {t.device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def check_workspace(t, name, nbytes, device):
+    """Raise ValueError unless `t` is a contiguous tensor on `device` holding at
+    least `nbytes` bytes; returns its size in bytes."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a tensor, got {type(t).__name__}")
+    if t.device != device:
+        raise ValueError(f"{name} must be on device {device}, got {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{name} holds {have} bytes, {nbytes} needed")
+    return have
+
+
+def _cuda_device(t, name):
+    """The CUDA device of input `t` (ValueError if it is not a CUDA tensor)."""
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA tensor")
+    return t.device
+
+
 def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
@@ -138,70 +181,79 @@ def plan(n, B=64, L=2, row_ptr=None, col_idx=None, stream=None):
     """Route table of Eq. 1 as device CSR (int32 row_ptr[NB+1], col_idx[nnz])."""
     import torch
     nb, nnz, _ = plan_size(n, B, L)
+    dev = torch.device("cuda", torch.cuda.current_device())
     if row_ptr is None:
-        row_ptr = torch.empty(nb + 1, dtype=torch.int32, device="cuda")
+        row_ptr = torch.empty(nb + 1, dtype=torch.int32, device=dev)
     if col_idx is None:
-        col_idx = torch.empty(max(nnz, 1), dtype=torch.int32, device="cuda")
-    for t in (row_ptr, col_idx):
-        if not (t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()):
-            raise ValueError("row_ptr / col_idx must be contiguous int32 CUDA tensors")
-    if row_ptr.numel() < nb + 1:
-        raise ValueError("row_ptr too small")
+        col_idx = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    check_buffer(row_ptr, "row_ptr", (nb + 1,), torch.int32, dev)
+    if col_idx.dim() != 1:
+        raise ValueError("col_idx must be 1-D")
+    check_buffer(col_idx, "col_idx", col_idx.shape, torch.int32, dev)
     _check(load().bf1_plan(int(n), int(B), int(L), _ptr(row_ptr), _ptr(col_idx),
                            col_idx.numel(), _stream(stream)), "bf1_plan")
     return row_ptr, col_idx[:nnz]
 
 
 def _prep(q, k, v, out, lse, want_lse):
+    """Check the attention operands and the caller's output buffers (or
+    allocate them) on q's device; returns (out, lse, sizes)."""
     import torch
-    for name, t in (("q", q), ("k", k), ("v", v)):
-        if not t.is_cuda or t.dtype != torch.bfloat16 or t.dim() != 4 or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous 4-D bf16 CUDA tensor")
+    dev = _cuda_device(q, "q")
+    if q.dim() != 4:
+        raise ValueError("q must be 4-D [batch, Hq, n, d]")
     batch, Hq, n, d = q.shape
-    if k.shape != v.shape or k.shape[0] != batch or k.shape[2] != n or k.shape[3] != d:
-        raise ValueError("k and v must be [batch, Hkv, n, d] matching q")
+    check_buffer(q, "q", q.shape, torch.bfloat16, dev)
+    if not isinstance(k, torch.Tensor) or k.dim() != 4:
+        raise ValueError("k must be a 4-D tensor [batch, Hkv, n, d]")
     Hkv = k.shape[1]
+    check_buffer(k, "k", (batch, Hkv, n, d), torch.bfloat16, dev)
+    check_buffer(v, "v", (batch, Hkv, n, d), torch.bfloat16, dev)
     if out is None:
         out = torch.empty_like(q)
-    elif out.shape != q.shape or out.dtype != torch.bfloat16 or not out.is_contiguous():
-        raise ValueError("out must be a contiguous bf16 tensor shaped like q")
+    check_buffer(out, "out", q.shape, torch.bfloat16, dev)
     if lse is None and want_lse:
-        lse = torch.empty((batch, Hq, n), dtype=torch.float32, device=q.device)
-    if lse is not None and (lse.shape != (batch, Hq, n) or lse.dtype != torch.float32
-                            or not lse.is_contiguous()):
-        raise ValueError("lse must be a contiguous float32 tensor [batch, Hq, n]")
+        lse = torch.empty((batch, Hq, n), dtype=torch.float32, device=dev)
+    if lse is not None:
+        check_buffer(lse, "lse", (batch, Hq, n), torch.float32, dev)
     return out, lse, (batch, n, Hq, Hkv, d)
 
 
 def attn_fwd(q, k, v, B=64, L=2, out=None, lse=None, want_lse=True, stream=None):
     """BF1 prefill forward; returns (O, LSE)."""
+    import torch
     out, lse, (batch, n, Hq, Hkv, d) = _prep(q, k, v, out, lse, want_lse)
-    _check(load().bf1_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch, n, Hq,
-                               Hkv, d, int(B), int(L), _stream(stream)), "bf1_attn_fwd")
+    with torch.cuda.device(q.device):
+        _check(load().bf1_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch, n, Hq,
+                                   Hkv, d, int(B), int(L), _stream(stream)), "bf1_attn_fwd")
     return out, lse
 
 
 def attn_fwd_csr(q, k, v, B, row_ptr, col_idx, out=None, lse=None, want_lse=True, stream=None):
     """Forward over a caller-supplied block route (CSR, int32 CUDA tensors)."""
     import torch
-    for t in (row_ptr, col_idx):
-        if not (t.is_cuda and t.dtype == torch.int32 and t.is_contiguous()):
-            raise ValueError("row_ptr / col_idx must be contiguous int32 CUDA tensors")
     out, lse, (batch, n, Hq, Hkv, d) = _prep(q, k, v, out, lse, want_lse)
+    if int(B) < 1:
+        raise ValueError("B must be positive")
     nb = -(-n // int(B))
-    if row_ptr.numel() < nb + 1:
-        raise ValueError("row_ptr must have ceil(n/B)+1 entries")
-    _check(load().bf1_attn_fwd_csr(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch, n,
-                                   Hq, Hkv, d, int(B), _ptr(row_ptr), _ptr(col_idx),
-                                   col_idx.numel(), _stream(stream)), "bf1_attn_fwd_csr")
+    check_buffer(row_ptr, "row_ptr", (nb + 1,), torch.int32, q.device)
+    if not isinstance(col_idx, torch.Tensor) or col_idx.dim() != 1:
+        raise ValueError("col_idx must be a 1-D tensor")
+    check_buffer(col_idx, "col_idx", col_idx.shape, torch.int32, q.device)
+    with torch.cuda.device(q.device):
+        _check(load().bf1_attn_fwd_csr(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch, n,
+                                       Hq, Hkv, d, int(B), _ptr(row_ptr), _ptr(col_idx),
+                                       col_idx.numel(), _stream(stream)), "bf1_attn_fwd_csr")
     return out, lse
 
 
 def dense_causal_fwd(q, k, v, out=None, lse=None, want_lse=True, stream=None):
     """In-house dense causal attention built from the same kernel."""
+    import torch
     out, lse, (batch, n, Hq, Hkv, d) = _prep(q, k, v, out, lse, want_lse)
-    _check(load().bf1_dense_causal_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch,
-                                       n, Hq, Hkv, d, _stream(stream)), "bf1_dense_causal_fwd")
+    with torch.cuda.device(q.device):
+        _check(load().bf1_dense_causal_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch,
+                                           n, Hq, Hkv, d, _stream(stream)), "bf1_dense_causal_fwd")
     return out, lse
 
 
@@ -277,25 +329,28 @@ def attn_bwd(q, k, v, o, do, lse, B=64, L=2, dq=None, dk=None, dv=None, workspac
     """BF1 backward; returns float32 (dQ, dK, dV).  o and lse are the
     forward's outputs; do is the upstream gradient of o (bf16, o's shape)."""
     import torch
-    out, _, (batch, n, Hq, Hkv, d) = _prep(q, k, v, o, lse, True)
-    if do.shape != q.shape or do.dtype != torch.bfloat16 or not do.is_contiguous() or not do.is_cuda:
-        raise ValueError("do must be a contiguous bf16 CUDA tensor shaped like q")
-    def _grad(t, shape):
+    if o is None or lse is None:
+        raise ValueError("attn_bwd needs the forward's o and lse")
+    _, _, (batch, n, Hq, Hkv, d) = _prep(q, k, v, o, lse, True)
+    dev = q.device
+    check_buffer(do, "do", q.shape, torch.bfloat16, dev)
+
+    def _grad(t, name, shape):
         if t is None:
-            return torch.empty(shape, dtype=torch.float32, device=q.device)
-        if t.shape != shape or t.dtype != torch.float32 or not t.is_contiguous():
-            raise ValueError("gradient buffers must be contiguous float32 tensors")
-        return t
-    dq = _grad(dq, q.shape)
-    dk = _grad(dk, k.shape)
-    dv = _grad(dv, v.shape)
+            return torch.empty(shape, dtype=torch.float32, device=dev)
+        return check_buffer(t, name, shape, torch.float32, dev)
+    dq = _grad(dq, "dq", q.shape)
+    dk = _grad(dk, "dk", k.shape)
+    dv = _grad(dv, "dv", v.shape)
     need = bwd_workspace_size(batch, n, Hq, Hkv, d, B, L)
     if workspace is None:
-        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=q.device)
-    _check(load().bf1_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq),
-                               _ptr(dk), _ptr(dv), batch, n, Hq, Hkv, d, int(B), int(L),
-                               _ptr(workspace), workspace.numel(), _stream(stream)),
-           "bf1_attn_bwd")
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    ws_bytes = check_workspace(workspace, "workspace", need, dev)
+    with torch.cuda.device(dev):
+        _check(load().bf1_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(do), _ptr(lse), _ptr(dq),
+                                   _ptr(dk), _ptr(dv), batch, n, Hq, Hkv, d, int(B), int(L),
+                                   _ptr(workspace), ws_bytes, _stream(stream)),
+               "bf1_attn_bwd")
     return dq, dk, dv
 
 
@@ -309,10 +364,13 @@ def decode_plan_stride(max_seq_len, B=64, L=2, dense=False):
     return out.value
 
 
-def _i32_cuda(t, name, dim):
+def _i32_cuda(t, name, dim, device=None):
     import torch
-    if not t.is_cuda or t.dtype != torch.int32 or t.dim() != dim or not t.is_contiguous():
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.int32 \
+            or t.dim() != dim or not t.is_contiguous():
         raise ValueError(f"{name} must be a contiguous {dim}-D int32 CUDA tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} must be on device {device}, got {t.device}")
 
 
 def decode_plan(seq_lens, page_table, num_pages, stride, B=64, L=2, dense=False, plan=None,
@@ -321,17 +379,18 @@ def decode_plan(seq_lens, page_table, num_pages, stride, B=64, L=2, dense=False,
     every sequence: the pages of its earlier selected blocks."""
     import torch
     _i32_cuda(seq_lens, "seq_lens", 1)
-    _i32_cuda(page_table, "page_table", 2)
+    dev = seq_lens.device
+    _i32_cuda(page_table, "page_table", 2, dev)
     batch, max_pages = page_table.shape
     if seq_lens.shape[0] != batch:
         raise ValueError("seq_lens and page_table disagree on the batch size")
     if plan is None:
-        plan = torch.empty((batch, stride), dtype=torch.int32, device=seq_lens.device)
-    elif plan.shape != (batch, stride) or plan.dtype != torch.int32 or not plan.is_contiguous():
-        raise ValueError("plan must be a contiguous int32 tensor [batch, stride]")
-    _check(load().bf1_decode_plan(batch, _ptr(seq_lens), _ptr(page_table), max_pages, int(num_pages),
-                                  int(B), int(L), int(bool(dense)), _ptr(plan), int(stride),
-                                  _stream(stream)), "bf1_decode_plan")
+        plan = torch.empty((batch, stride), dtype=torch.int32, device=dev)
+    check_buffer(plan, "plan", (batch, stride), torch.int32, dev)
+    with torch.cuda.device(dev):
+        _check(load().bf1_decode_plan(batch, _ptr(seq_lens), _ptr(page_table), max_pages,
+                                      int(num_pages), int(B), int(L), int(bool(dense)), _ptr(plan),
+                                      int(stride), _stream(stream)), "bf1_decode_plan")
     return plan
 
 
@@ -347,27 +406,36 @@ def attn_decode(q, k_pages, v_pages, seq_lens, plan, B=64, out=None, lse=None, w
     """Attention of each sequence's newest token over the paged cache, using
     a decode plan; returns (O [batch, Hq, d] bf16, LSE [batch, Hq] fp32)."""
     import torch
-    for name, t, dim in (("q", q, 3), ("k_pages", k_pages, 4), ("v_pages", v_pages, 4)):
-        if not t.is_cuda or t.dtype != torch.bfloat16 or t.dim() != dim or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous {dim}-D bf16 CUDA tensor")
+    dev = _cuda_device(q, "q")
+    if q.dim() != 3:
+        raise ValueError("q must be 3-D [batch, Hq, d]")
     batch, Hq, d = q.shape
+    check_buffer(q, "q", q.shape, torch.bfloat16, dev)
+    if not isinstance(k_pages, torch.Tensor) or k_pages.dim() != 4:
+        raise ValueError("k_pages must be a 4-D tensor [num_pages, Hkv, B, d]")
     num_pages, Hkv, pw, dk = k_pages.shape
-    if v_pages.shape != k_pages.shape or dk != d or pw != B:
+    if dk != d or pw != B:
         raise ValueError("k_pages / v_pages must be [num_pages, Hkv, B, d] matching q")
-    _i32_cuda(seq_lens, "seq_lens", 1)
-    _i32_cuda(plan, "plan", 2)
+    check_buffer(k_pages, "k_pages", k_pages.shape, torch.bfloat16, dev)
+    check_buffer(v_pages, "v_pages", k_pages.shape, torch.bfloat16, dev)
+    _i32_cuda(seq_lens, "seq_lens", 1, dev)
+    _i32_cuda(plan, "plan", 2, dev)
     if seq_lens.shape[0] != batch or plan.shape[0] != batch:
         raise ValueError("batch sizes disagree")
     if out is None:
         out = torch.empty_like(q)
+    check_buffer(out, "out", q.shape, torch.bfloat16, dev)
     if lse is None:
-        lse = torch.empty((batch, Hq), dtype=torch.float32, device=q.device)
+        lse = torch.empty((batch, Hq), dtype=torch.float32, device=dev)
+    check_buffer(lse, "lse", (batch, Hq), torch.float32, dev)
     stride = plan.shape[1]
     need = decode_workspace_size(batch, Hq, Hkv, d, stride)
     if workspace is None:
-        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
-    _check(load().bf1_decode_attn(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(seq_lens), num_pages,
-                                  _ptr(plan), stride, _ptr(out), _ptr(lse), batch, Hq, Hkv, d, int(B),
-                                  _ptr(workspace), workspace.numel(), _stream(stream)), "bf1_decode_attn")
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    ws_bytes = check_workspace(workspace, "workspace", need, dev)
+    with torch.cuda.device(dev):
+        _check(load().bf1_decode_attn(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(seq_lens), num_pages,
+                                      _ptr(plan), stride, _ptr(out), _ptr(lse), batch, Hq, Hkv, d,
+                                      int(B), _ptr(workspace), ws_bytes, _stream(stream)),
+               "bf1_decode_attn")
     return out, lse
-
