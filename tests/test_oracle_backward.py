@@ -152,3 +152,59 @@ def test_abs_terms_bound_the_gradients():
     t = orc.attn_bwd_abs_terms_fp64(q, k, v, w, b, L)
     for x, y in zip(g, t):
         assert (np.abs(x) <= y + 1e-12).all()
+
+
+# ---------------------------------------------------------------------------
+# Tightness of the term-magnitude sums (the backward's element-wise error
+# scale): they must equal the hand-worked values, and they must be attained
+# exactly when every term of a gradient element has the same sign.
+# ---------------------------------------------------------------------------
+
+def _hand_case(case):
+    V = np.array([[1, 0], [0, 1], [1, 1.0]])
+    dO = np.array([[1, 0], [0, 2], [1, -1.0]])
+    K = np.array([[1, 2], [3, -1], [-2, 1.0]])
+    Q = np.array([[2, 1], [1, -1], [0, 3.0]])
+    q, k = (np.zeros((3, 2)), K) if case == "A" else (Q, np.zeros((3, 2)))
+    return [x[None, None] for x in (q, k, V, dO)]
+
+
+def test_abs_terms_hand_worked(golden):
+    from fractions import Fraction
+    rows = golden("bwd_abs_terms_hand.txt")
+    assert len(rows) == 16
+    c = 1 / math.sqrt(2)
+    for case, kind, grad, row, a, b, times in rows:
+        q, k, v, do = _hand_case(case)
+        got = orc.attn_bwd_abs_terms_fp64(q, k, v, do, 4, 2, kind=kind)
+        g = {"dQ": got[0], "dK": got[1], "dV": got[2]}[grad][0, 0, int(row)]
+        want = np.array([float(Fraction(a)), float(Fraction(b))]) * (c if times == "c" else 1.0)
+        np.testing.assert_allclose(g, want, rtol=0, atol=1e-14, err_msg=f"{case} {kind} {grad} {row}")
+
+
+def test_abs_terms_dv_attained_for_nonnegative_upstream():
+    # With dO >= 0 every term P_ts dO_t of dV_s is non-negative, so the sum of
+    # magnitudes is the gradient itself.
+    n, b, L = 90, 8, 2
+    q, k, v, w = _rand(23, 1, 4, 2, n, 5)
+    w = np.abs(w)
+    _, _, dv = orc.attn_bwd_gathered_fp64(q, k, v, w, b, L)
+    _, _, tv = orc.attn_bwd_abs_terms_fp64(q, k, v, w, b, L)
+    np.testing.assert_allclose(tv, np.abs(dv), rtol=1e-12, atol=1e-14)
+
+
+def test_abs_terms_dq_attained_for_one_sign_per_row():
+    # Two keys per query row (block width 1, route {0, j} at L = 0 only for
+    # j = 1): dS of row 1 is (-x, +x).  With K_0 <= 0 <= K_1 both terms of
+    # dQ_1 = c (dS_10 K_0 + dS_11 K_1) share a sign in every column, so the
+    # sum of magnitudes equals |dQ_1|.
+    rng = np.random.default_rng(29)
+    q = rng.standard_normal((1, 1, 2, 4))
+    k = np.stack([-np.abs(rng.standard_normal(4)), np.abs(rng.standard_normal(4))])[None, None]
+    v = rng.standard_normal((1, 1, 2, 4))
+    do = rng.standard_normal((1, 1, 2, 4))
+    dq, _, _ = orc.attn_bwd_gathered_fp64(q, k, v, do, 1, 0)
+    tq, _, _ = orc.attn_bwd_abs_terms_fp64(q, k, v, do, 1, 0)
+    p_ds = np.sign(dq[0, 0, 1])
+    assert np.all(p_ds != 0)
+    np.testing.assert_allclose(tq[0, 0, 1], np.abs(dq[0, 0, 1]), rtol=1e-12)

@@ -174,6 +174,45 @@ def test_backward_mutations_are_caught(monkeypatch, bad):
     assert run_pins(BWD_PINS)
 
 
+# ---- backward error scale: planted slips in the term-magnitude sums --------
+from conftest import read_golden  # noqa: E402
+
+
+def terms_unscaled(qr, kr, vr, dor, allowed, scale, delta=None):
+    # c dropped from the dQ and dK terms
+    p, dp, delta = _bwd_parts(qr, kr, vr, dor, allowed, scale)
+    a = np.abs(p * (dp - delta))
+    return a @ np.abs(kr), a.T @ np.abs(qr), p.T @ np.abs(dor)
+
+
+def terms_p_for_ds(qr, kr, vr, dor, allowed, scale, delta=None):
+    # |dS| replaced by P
+    p, dp, delta = _bwd_parts(qr, kr, vr, dor, allowed, scale)
+    return scale * (p @ np.abs(kr)), scale * (p.T @ np.abs(qr)), p.T @ np.abs(dor)
+
+
+def terms_pdp_without_p(qr, kr, vr, dor, allowed, scale, delta=None):
+    # P dropped from the cancellation scale P (|dP| + |D|)
+    p, dp, delta = _bwd_parts(qr, kr, vr, dor, allowed, scale)
+    a = np.where(allowed, np.abs(dp) + np.abs(delta), 0.0)
+    return scale * (a @ np.abs(kr)), scale * (a.T @ np.abs(qr)), np.zeros((kr.shape[0], dor.shape[1]))
+
+
+TERM_PINS = [
+    (TB.test_abs_terms_hand_worked, (read_golden,)),
+    (TB.test_abs_terms_dv_attained_for_nonnegative_upstream, ()),
+    (TB.test_abs_terms_dq_attained_for_one_sign_per_row, ()),
+]
+
+
+@pytest.mark.parametrize("name,bad", [("_bwd_abs_terms", terms_unscaled),
+                                      ("_bwd_abs_terms", terms_p_for_ds),
+                                      ("_bwd_abs_terms_pdp", terms_pdp_without_p)])
+def test_backward_error_scale_mutations_are_caught(monkeypatch, name, bad):
+    monkeypatch.setattr(orc, name, bad)
+    assert run_pins(TERM_PINS)
+
+
 # ---------------------------------------------------------------------------
 # Route variants and the depth search
 # ---------------------------------------------------------------------------
