@@ -318,6 +318,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
         for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
     float m_run = -1e30f;  // running max, log2 units (finite: masked scores give 0)
     float l_run = 0.f;     // this lane's partial row sum (its 32 keys of each tile)
+    float l_bf = 0.f;      // the same sum over the bf16-rounded weights the PV product uses
 
     // ---- prologue: K0, V0 and K1 resident, S0 computed ----------------------
     int32_t ti0 = 0, ti1 = 0, ti2 = 0;
@@ -378,6 +379,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
             const float alpha = need ? __builtin_amdgcn_exp2f(m_run - m_cand) : 1.0f;
             m_run = need ? m_cand : m_run;
             l_run *= alpha;
+            l_bf *= alpha;
 #pragma unroll
             for (int t = 0; t < DT; ++t)
 #pragma unroll
@@ -468,6 +470,18 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
             }
         }
         l_run += ls0 + ls1;
+        {   // the bf16 weights as the PV product will see them, summed in fp32
+            const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+            float lb0 = 0.f, lb1 = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                lb0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[t][0], pb[t][1]}, ones, lb0, false);
+                lb1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[t][2], pb[t][3]}, ones, lb1, false);
+                lb0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[t][4], pb[t][5]}, ones, lb0, false);
+                lb1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[t][6], pb[t][7]}, ones, lb1, false);
+            }
+            l_bf += lb0 + lb1;
+        }
         __builtin_amdgcn_s_setprio(0);
 
         // phase 2: O^T += V^T P^T (transpose reads of V_k), interleaved with the
@@ -504,7 +518,13 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
            step(std::integral_constant<int, 1>{}, s_b, s_a)) {
     }
 
-    // ---- epilogue: O = acc / l, LSE = (m + log2 l) ln 2 ---------------------
+    // ---- epilogue: O = acc / l_bf, LSE = (m + log2 l) ln 2 ------------------
+    // O is normalised by the sum of the weights exactly as the PV product used
+    // them (bf16), so the weights it applies sum to one: a row dominated by
+    // one key reproduces that key's value row without the rounding error of
+    // its weight (which, with the output's own bf16 rounding, could exceed
+    // 2e-2 for |V| near 5).  The LSE keeps the fp32 sum, whose relative error
+    // stays near 1e-7 where the bf16 sum's can reach 2^-9.
     // O goes through LDS so that the global stores are whole rows: the
     // accumulator holds, per lane, 8-byte pieces of one query row; each wave
     // writes its 32 x D tile into its own slice of the (now idle) K buffers,
@@ -515,7 +535,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     // non-temporal: O is not read again here, and streaming it through L2
     // evicted K/V tiles that other workgroups were still reusing.
     const float l_tot = pair_sum(l_run);
-    const float inv = 1.f / l_tot;
+    const float inv = 1.f / pair_sum(l_bf);
     constexpr int OCH = D / 8;                 // 16-byte chunks per row
     char* oslice = reinterpret_cast<char*>(&sm.k[0][0]) + wave * 32 * RB;
 #pragma unroll

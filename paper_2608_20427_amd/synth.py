@@ -96,6 +96,30 @@ def make_qkv(w, device="cpu"):
     return tq, tk, tv
 
 
+def make_qkv_large_logits(w, q_mul=8.0, k_ramp=9.0, diag=0.0, device="cpu"):
+    """Inputs with scores in the hundreds whose row maximum keeps growing
+    along a row: Q ~ q_mul N(0, 1) and K[s] ~ (1 + k_ramp s / n) N(0, 1), so
+    later key blocks carry larger scores and a route visited in ascending
+    block order sees its running maximum jump many times.  With diag > 0,
+    K[s] also gets diag * (1 + k_ramp s / n) * sign(sum of the group's Q[s])
+    added, which makes the diagonal key the largest score of most rows: the
+    row maximum then arrives in the self block, visited last.  V ~ N(0, 1).
+    All drawn as float32 on the host (PCG64 of the workload seed, stream 2)
+    and rounded to bf16."""
+    rng = np.random.Generator(np.random.PCG64([w.seed, 2]))
+    q = rng.standard_normal((w.batch, w.Hq, w.n, w.d), dtype=np.float32) * np.float32(q_mul)
+    k = rng.standard_normal((w.batch, w.Hkv, w.n, w.d), dtype=np.float32)
+    if diag > 0.0:
+        G = w.Hq // w.Hkv
+        qsum = q.reshape(w.batch, w.Hkv, G, w.n, w.d).sum(axis=2)
+        k += np.float32(diag) * np.sign(qsum).astype(np.float32)
+    ramp = (1.0 + k_ramp * np.arange(w.n, dtype=np.float64) / max(w.n, 1)).astype(np.float32)
+    k *= ramp[None, None, :, None]
+    v = rng.standard_normal((w.batch, w.Hkv, w.n, w.d), dtype=np.float32)
+    out = [torch.from_numpy(x).to(torch.bfloat16) for x in (q, k, v)]
+    return tuple(t.to(device) if device != "cpu" else t for t in out)
+
+
 def make_grad_out(w, device="cpu"):
     """Upstream gradient dO for workload ``w`` (bf16, Q's shape): standard
     normal from its own seeded stream (PCG64 of the workload seed, stream 1),
