@@ -24,6 +24,14 @@
  *    written in that case.
  *  - All tensors are caller-owned device memory on the current device.  The
  *    library never frees caller memory; it owns only its plan cache.
+ *  - Graph capture: bf1_attn_fwd and bf1_attn_bwd build the route plan of a
+ *    new (device, n, B, L) on first use (device allocation, a planner kernel
+ *    on a private stream and a host wait, so a cached plan is complete and
+ *    later calls add no stream dependency).  That first call cannot be
+ *    captured: made while `stream` is being captured it returns
+ *    BF1_ERR_CAPTURE and enqueues nothing.  Once the plan exists, calls can be
+ *    captured; a captured graph keeps pointing at the plan's memory, so
+ *    bf1_release_plans must not run while such a graph may still replay.
  *  - Layouts (row-major, contiguous):
  *        Q, O : [batch, Hq,  n, head_dim] bf16
  *        K, V : [batch, Hkv, n, head_dim] bf16
@@ -52,7 +60,8 @@ typedef enum {
     BF1_ERR_UNSUPPORTED = -2,      /* valid but not built: head_dim, B, group */
     BF1_ERR_BUFFER_TOO_SMALL = -3, /* col_capacity below the route size */
     BF1_ERR_HIP = -4,              /* a HIP runtime call or launch failed */
-    BF1_ERR_NOMEM = -5             /* device allocation for the plan cache failed */
+    BF1_ERR_NOMEM = -5,            /* device allocation for the plan cache failed */
+    BF1_ERR_CAPTURE = -6           /* a plan would have to be built during graph capture */
 } bf1_status;
 
 /*
@@ -95,15 +104,21 @@ int bf1_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
                  int32_t B, int32_t L, void* stream);
 
 /*
- * The same kernel with a caller-supplied route table (any block route in
- * the CSR form written by bf1_plan; used for route variants and tests).
+ * The same kernel with a caller-supplied route table: any causal block route
+ * in the CSR form written by bf1_plan.  The paper times BF1 against other
+ * routes of the same selected-pair count through one kernel (§4.3, §5.1:
+ * matched local sliding and a static random graph; bf1_plan_variant builds
+ * them), so the kernel takes the table as data.
  *   row_ptr : device int32[ceil(n/B) + 1], non-decreasing.
  *   col_idx : device int32[nnz]; entries of row j name key blocks.
- * Row ranges are clamped to [0, nnz]; entries outside [0, j] are ignored
- * (the route is causal: the self block j gets the token-level triangle,
- * earlier blocks are fully visible).  Each block should appear at most once
- * per row, and rows that name no block at all produce undefined values (never
- * an out-of-bounds access).  All memory stays caller-owned.
+ *   nnz     : the number of entries col_idx holds.  This argument is not in
+ *             bf1_attn_fwd's interface: a table the caller wrote is not
+ *             trusted, so the kernel clamps every row range to [0, nnz] and
+ *             can never read past the end of col_idx, whatever row_ptr says.
+ * Entries outside [0, j] are ignored (the route is causal: the self block j
+ * gets the token-level triangle, earlier blocks are fully visible).  Each
+ * block should appear at most once per row; a row that names no block at
+ * all gets O = 0 and LSE = -inf.  All memory stays caller-owned.
  */
 int bf1_attn_fwd_csr(const void* Q, const void* K, const void* V, void* O, float* LSE,
                      int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,

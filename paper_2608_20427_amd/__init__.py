@@ -30,6 +30,7 @@ BF1_ERR_UNSUPPORTED = -2
 BF1_ERR_BUFFER_TOO_SMALL = -3
 BF1_ERR_HIP = -4
 BF1_ERR_NOMEM = -5
+BF1_ERR_CAPTURE = -6
 
 
 class BF1Error(RuntimeError):

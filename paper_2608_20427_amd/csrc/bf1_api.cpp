@@ -16,7 +16,7 @@
 
 namespace {
 
-constexpr int kVersion = 10100;  // 1.1.0
+constexpr int kVersion = 10200;  // 1.2.0
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -29,17 +29,29 @@ bool route_sizes(int64_t n, int64_t B, int64_t L, int64_t* NB, int64_t* nnz) {
 }
 
 // ---- plan cache: (device, n, B, L) -> device CSR --------------------------
+// A plan is complete before it enters the cache (built on a private stream
+// that the host waits for), so later calls use it with no stream ordering at
+// all -- which also makes them safe to capture into a HIP graph.  Building a
+// plan is refused while the caller's stream is being captured.
 struct Plan {
     int32_t* row_ptr = nullptr;
     int32_t* col_idx = nullptr;
     int64_t nnz = 0;
-    hipEvent_t ready = nullptr;  // recorded after the planner kernel
 };
 
 std::mutex g_mu;
 std::map<std::tuple<int, int64_t, int32_t, int32_t>, Plan> g_plans;
+std::map<int, hipStream_t> g_plan_streams;  // per device, created on first use
 
 int status_of(hipError_t e) { return e == hipSuccess ? BF1_OK : BF1_ERR_HIP; }
+
+// True (and BF1_OK) if `s` is being captured into a graph.
+int capturing(hipStream_t s, bool* yes) {
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &st) != hipSuccess) return BF1_ERR_HIP;
+    *yes = st != hipStreamCaptureStatusNone;
+    return BF1_OK;
+}
 
 // Validation shared by the attention entry points.
 int check_attn(const void* Q, const void* K, const void* V, void* O, float* LSE, int32_t batch,
@@ -99,44 +111,48 @@ int64_t decode_ws_bytes(int64_t batch, int64_t Hq, int64_t Hkv, int64_t D, int64
 int run_attn(const bf1::AttnArgs& a, hipStream_t s) { return status_of(bf1::launch_attention(a, s)); }
 
 // Cached forward route of (current device, n, B, L), built by the planner
-// kernel on first use; `s` is ordered after the planner.
+// kernel on first use and complete on return.  `s` is the caller's stream
+// (only checked for capture).
 int get_plan(int64_t n, int32_t B, int32_t L, hipStream_t s, Plan* out) {
     int64_t NB, nnz;
     if (!route_sizes(n, B, L, &NB, &nnz)) return BF1_ERR_INVALID_ARG;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return BF1_ERR_HIP;
-    {
-        std::lock_guard<std::mutex> lock(g_mu);
-        auto key = std::make_tuple(dev, n, B, L);
-        auto it = g_plans.find(key);
-        if (it == g_plans.end()) {
-            Plan p;
-            p.nnz = nnz;
-            if (hipMalloc((void**)&p.row_ptr, sizeof(int32_t) * (NB + 1)) != hipSuccess)
-                return BF1_ERR_NOMEM;
-            if (hipMalloc((void**)&p.col_idx, sizeof(int32_t) * (nnz > 0 ? nnz : 1)) != hipSuccess) {
-                (void)hipFree(p.row_ptr);
-                return BF1_ERR_NOMEM;
-            }
-            if (hipEventCreateWithFlags(&p.ready, hipEventDisableTiming) != hipSuccess) {
-                (void)hipFree(p.row_ptr);
-                (void)hipFree(p.col_idx);
-                return BF1_ERR_HIP;
-            }
-            hipError_t e = bf1::launch_plan((int32_t)NB, L, p.row_ptr, p.col_idx, s);
-            if (e == hipSuccess) e = hipEventRecord(p.ready, s);
-            if (e != hipSuccess) {
-                (void)hipFree(p.row_ptr);
-                (void)hipFree(p.col_idx);
-                (void)hipEventDestroy(p.ready);
-                return BF1_ERR_HIP;
-            }
-            it = g_plans.emplace(key, p).first;
-        }
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto key = std::make_tuple(dev, n, B, L);
+    auto it = g_plans.find(key);
+    if (it != g_plans.end()) {
         *out = it->second;
+        return BF1_OK;
     }
-    // The plan may have been built on another stream: order this one after it.
-    if (hipStreamWaitEvent(s, out->ready, 0) != hipSuccess) return BF1_ERR_HIP;
+    bool cap = false;
+    int st = capturing(s, &cap);
+    if (st != BF1_OK) return st;
+    if (cap) return BF1_ERR_CAPTURE;
+    hipStream_t ps = nullptr;
+    auto ps_it = g_plan_streams.find(dev);
+    if (ps_it == g_plan_streams.end()) {
+        if (hipStreamCreateWithFlags(&ps, hipStreamNonBlocking) != hipSuccess) return BF1_ERR_HIP;
+        g_plan_streams.emplace(dev, ps);
+    } else {
+        ps = ps_it->second;
+    }
+    Plan p;
+    p.nnz = nnz;
+    if (hipMalloc((void**)&p.row_ptr, sizeof(int32_t) * (NB + 1)) != hipSuccess) return BF1_ERR_NOMEM;
+    if (hipMalloc((void**)&p.col_idx, sizeof(int32_t) * (nnz > 0 ? nnz : 1)) != hipSuccess) {
+        (void)hipFree(p.row_ptr);
+        return BF1_ERR_NOMEM;
+    }
+    hipError_t e = bf1::launch_plan((int32_t)NB, L, p.row_ptr, p.col_idx, ps);
+    if (e == hipSuccess) e = hipStreamSynchronize(ps);
+    if (e != hipSuccess) {
+        (void)hipFree(p.row_ptr);
+        (void)hipFree(p.col_idx);
+        return BF1_ERR_HIP;
+    }
+    g_plans.emplace(key, p);
+    *out = p;
     return BF1_OK;
 }
 
@@ -221,13 +237,17 @@ int bwd_workspace_bytes(int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32
     return BF1_OK;
 }
 
-int get_bwd_plan(int64_t n, int32_t B, int32_t L, BwdPlan* out) {
+int get_bwd_plan(int64_t n, int32_t B, int32_t L, hipStream_t s, BwdPlan* out) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return BF1_ERR_HIP;
     std::lock_guard<std::mutex> lock(g_mu);
     auto key = std::make_tuple(dev, n, B, L);
     auto it = g_bwd_plans.find(key);
     if (it == g_bwd_plans.end()) {
+        bool cap = false;
+        int st = capturing(s, &cap);
+        if (st != BF1_OK) return st;
+        if (cap) return BF1_ERR_CAPTURE;
         BwdLayout lay;
         if (!bwd_layout(n, B, L, &lay, true)) return BF1_ERR_INVALID_ARG;
         BwdPlan p;
@@ -271,6 +291,9 @@ const char* bf1_status_string(int status) {
         case BF1_ERR_BUFFER_TOO_SMALL: return "BF1_ERR_BUFFER_TOO_SMALL: route table capacity too small";
         case BF1_ERR_HIP: return "BF1_ERR_HIP: HIP runtime or launch error";
         case BF1_ERR_NOMEM: return "BF1_ERR_NOMEM: device allocation failed";
+        case BF1_ERR_CAPTURE:
+            return "BF1_ERR_CAPTURE: the route plan is not built yet and cannot be built while the "
+                   "stream is being captured (call once outside capture first)";
         default: return "BF1: unknown status";
     }
 }
@@ -472,7 +495,7 @@ int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, con
     st = get_plan(n, B, L, s, &plan);
     if (st != BF1_OK) return st;
     BwdPlan bp;
-    st = get_bwd_plan(n, B, L, &bp);
+    st = get_bwd_plan(n, B, L, s, &bp);
     if (st != BF1_OK) return st;
     const int64_t delta_bytes = ((int64_t)batch * Hq * n * 4 + 255) / 256 * 256;
     float* delta = (float*)workspace;
@@ -488,14 +511,12 @@ int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, con
 
 void bf1_release_plans(void) {
     std::lock_guard<std::mutex> lock(g_mu);
+    if (!g_plans.empty() || !g_bwd_plans.empty()) (void)hipDeviceSynchronize();
     for (auto& kv : g_plans) {
-        (void)hipEventSynchronize(kv.second.ready);
         (void)hipFree(kv.second.row_ptr);
         (void)hipFree(kv.second.col_idx);
-        (void)hipEventDestroy(kv.second.ready);
     }
     g_plans.clear();
-    if (!g_bwd_plans.empty()) (void)hipDeviceSynchronize();
     for (auto& kv : g_bwd_plans) {
         (void)hipFree(kv.second.users);
         (void)hipFree(kv.second.uoffs);

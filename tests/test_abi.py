@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_status_strings(lib):
-    for st in range(-5, 1):
+    for st in range(-6, 1):
         assert bf1.status_string(st).startswith("BF1")
     assert "unknown" in bf1.status_string(42)
     assert bf1.version() >= 10000

@@ -267,11 +267,15 @@ def test_decode_workspace_too_small_and_lse_optional():
     plan = bf1.decode_plan(dev["sl"], dev["table"], dev["num_pages"], dev["stride"], 64, 2)
     need = bf1.decode_workspace_size(2, 4, 2, 128, dev["stride"])
     ws = torch.empty(need - 256, dtype=torch.uint8, device="cuda")
-    with pytest.raises(bf1.BF1Error) as e:
+    with pytest.raises(ValueError):     # the binding refuses it before the library
         bf1.attn_decode(dev["q"], dev["kp"], dev["vp"], dev["sl"], plan, 64, workspace=ws)
-    assert e.value.status == bf1.BF1_ERR_BUFFER_TOO_SMALL
-    o1, l1, _ = run_decode(w, dev, plan=plan)
     lib = bf1.load()
+    o0 = torch.empty_like(dev["q"])
+    st = lib.bf1_decode_attn(bf1._ptr(dev["q"]), bf1._ptr(dev["kp"]), bf1._ptr(dev["vp"]), bf1._ptr(dev["sl"]),
+                             dev["num_pages"], bf1._ptr(plan), dev["stride"], bf1._ptr(o0), None, 2, 4, 2, 128,
+                             64, bf1._ptr(ws), need - 256, bf1._stream(None))
+    assert st == bf1.BF1_ERR_BUFFER_TOO_SMALL   # ... and so does the C ABI
+    o1, l1, _ = run_decode(w, dev, plan=plan)
     o2 = torch.empty_like(o1)
     ws = torch.empty(need, dtype=torch.uint8, device="cuda")
     st = lib.bf1_decode_attn(bf1._ptr(dev["q"]), bf1._ptr(dev["kp"]), bf1._ptr(dev["vp"]), bf1._ptr(dev["sl"]),

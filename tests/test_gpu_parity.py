@@ -387,3 +387,70 @@ def test_csr_out_of_range_entries_are_ignored():
     o2, l2 = bf1.attn_fwd(q, k, v, B=B, L=2)
     torch.cuda.synchronize()
     assert torch.equal(o, o2) and torch.equal(l, l2)
+
+
+# ---------------------------------------------------------------------------
+# Graph capture of the cached-plan entry points
+# ---------------------------------------------------------------------------
+
+def test_forward_and_backward_replay_in_a_graph():
+    # Plans are built by an eager call first; the forward and the backward are
+    # then captured into one graph and replayed several times, with eager work
+    # and synchronisations between replays.  Every replay equals the eager
+    # result bitwise.
+    w = synth.Workload("graph", 2, 1337, 4, 2, 128, 64, 2, seed=41)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    do = synth.make_grad_out(w, device="cuda")
+    o_e, l_e = bf1.attn_fwd(q, k, v)
+    g_e = bf1.attn_bwd(q, k, v, o_e, do, l_e)
+    torch.cuda.synchronize()
+    o, lse = torch.empty_like(o_e), torch.empty_like(l_e)
+    dq, dk, dv = (torch.empty_like(t) for t in g_e)
+    ws = torch.empty(bf1.bwd_workspace_size(2, 1337, 4, 2, 128, 64, 2), dtype=torch.uint8, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        bf1.attn_fwd(q, k, v, out=o, lse=lse)      # warm on the capture stream
+        bf1.attn_bwd(q, k, v, o, do, lse, dq=dq, dk=dk, dv=dv, workspace=ws)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        bf1.attn_fwd(q, k, v, out=o, lse=lse)
+        bf1.attn_bwd(q, k, v, o, do, lse, dq=dq, dk=dk, dv=dv, workspace=ws)
+    for rep in range(4):
+        for t in (o, lse, dq, dk, dv):
+            t.fill_(float("nan"))
+        x = bf1.attn_fwd(q[:, :, :500].contiguous(), k[:, :, :500].contiguous(),
+                         v[:, :, :500].contiguous())   # unrelated eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o, o_e) and torch.equal(lse, l_e), rep
+        for a, b in zip((dq, dk, dv), g_e):
+            assert torch.equal(a, b), rep
+        del x
+
+
+@pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")
+def test_first_call_under_capture_is_refused():
+    # A plan that does not exist yet cannot be built inside a capture: the call
+    # returns BF1_ERR_CAPTURE and enqueues nothing; afterwards the eager call
+    # builds the plan and works.
+    n = 1201
+    w = synth.Workload("cold", 1, n, 2, 1, 128, 64, 3, seed=42)
+    q, k, v = synth.make_qkv(w, device="cuda")
+    bf1.release_plans()
+    o = torch.empty_like(q)
+    lse = torch.empty((1, 2, n), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with pytest.raises(bf1.BF1Error) as e:
+        with torch.cuda.graph(graph):
+            bf1.attn_fwd(q, k, v, B=64, L=3, out=o, lse=lse)
+    assert e.value.status == bf1.BF1_ERR_CAPTURE
+    torch.cuda.synchronize()
+    o2, l2 = bf1.attn_fwd(q, k, v, B=64, L=3)
+    torch.cuda.synchronize()
+    o_ref, l_ref = orc.attn_gathered_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), 64, 3)
+    compare(o2, l2, o_ref, l_ref, tag="after refused capture")
