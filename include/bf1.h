@@ -104,6 +104,28 @@ int bf1_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
                  int32_t B, int32_t L, void* stream);
 
 /*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the BF1
+ * prefill forward of bf1_attn_fwd, same arguments, same kernels and bitwise
+ * the same results, with no allocation and no plan cache.  Each call runs the
+ * route planner into a fixed scratch array owned by the library (one
+ * 4 MiB __device__ array of int32, 2^20 entries, per device, held until the
+ * process ends) and then the attention kernel over that table, both on
+ * `stream`.  The table must fit: NB + 1 + nnz <= 2^20 (bf1_plan_size gives
+ * NB and nnz; at B = 64, L = 2 this allows n up to about 2M tokens), else
+ * BF1_ERR_BUFFER_TOO_SMALL is returned before anything is enqueued.  No
+ * scratch content needs clearing: the planner rewrites every entry the
+ * kernel reads.  All calls on one device share its array, so calls that
+ * overlap in time on one device (on different streams, or from several
+ * threads without ordering) race and may read each other's tables; calls
+ * ordered on one stream do not.  The first call on a device looks the
+ * array's address up (no allocation).
+ */
+int bf1_attn_fwd_noalloc(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                         int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                         int32_t B, int32_t L, void* stream);
+
+/*
  * The same kernel with a caller-supplied route table: any causal block route
  * in the CSR form written by bf1_plan.  The paper times BF1 against other
  * routes of the same selected-pair count through one kernel (§4.3, §5.1:

@@ -18,7 +18,7 @@ import os
 __all__ = [
     "BF1Error", "lib_path", "load", "version", "status_string", "plan_size", "plan",
     "attn_fwd", "attn_fwd_csr", "dense_causal_fwd", "release_plans", "selected_flops",
-    "plan_transposed", "bwd_workspace_size", "attn_bwd", "selected_bwd_flops",
+    "plan_transposed", "bwd_workspace_size", "attn_bwd", "selected_bwd_flops", "attn_fwd_noalloc",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -66,6 +66,8 @@ def load():
     attn = [vp, vp, vp, vp, vp, i32, i64, i32, i32, i32]
     lib.bf1_attn_fwd.restype = ctypes.c_int
     lib.bf1_attn_fwd.argtypes = attn + [i32, i32, vp]
+    lib.bf1_attn_fwd_noalloc.restype = ctypes.c_int
+    lib.bf1_attn_fwd_noalloc.argtypes = attn + [i32, i32, vp]
     lib.bf1_attn_fwd_csr.restype = ctypes.c_int
     lib.bf1_attn_fwd_csr.argtypes = attn + [i32, vp, vp, i64, vp]
     lib.bf1_dense_causal_fwd.restype = ctypes.c_int
@@ -227,6 +229,21 @@ def attn_fwd(q, k, v, B=64, L=2, out=None, lse=None, want_lse=True, stream=None)
     with torch.cuda.device(q.device):
         _check(load().bf1_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch, n, Hq,
                                    Hkv, d, int(B), int(L), _stream(stream)), "bf1_attn_fwd")
+    return out, lse
+
+
+def attn_fwd_noalloc(q, k, v, out, lse=None, B=64, L=2, stream=None):
+    """BF1 prefill forward that allocates no device memory (the route table
+    goes to the library's fixed scratch array): the caller passes O (and
+    optionally LSE); returns (O, LSE)."""
+    import torch
+    if out is None:
+        raise ValueError("attn_fwd_noalloc writes into a caller-provided out")
+    out, lse, (batch, n, Hq, Hkv, d) = _prep(q, k, v, out, lse, False)
+    with torch.cuda.device(q.device):
+        _check(load().bf1_attn_fwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), batch, n,
+                                           Hq, Hkv, d, int(B), int(L), _stream(stream)),
+               "bf1_attn_fwd_noalloc")
     return out, lse
 
 

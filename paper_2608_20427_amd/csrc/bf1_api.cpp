@@ -338,6 +338,29 @@ int bf1_attn_fwd(const void* Q, const void* K, const void* V, void* O, float* LS
     return run_attn(a, s);
 }
 
+int bf1_attn_fwd_noalloc(const void* Q, const void* K, const void* V, void* O, float* LSE,
+                         int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
+                         int32_t B, int32_t L, void* stream) {
+    int st = check_attn(Q, K, V, O, LSE, batch, n, Hq, Hkv, head_dim);
+    if (st != BF1_OK) return st;
+    if (L < 0) return BF1_ERR_INVALID_ARG;
+    if (B != 64 && B != 128) return BF1_ERR_UNSUPPORTED;
+    if (batch == 0 || n == 0) return BF1_OK;
+    int64_t NB, nnz;
+    if (!route_sizes(n, B, L, &NB, &nnz)) return BF1_ERR_INVALID_ARG;
+    if (NB + 1 + nnz > bf1::kNoallocInts) return BF1_ERR_BUFFER_TOO_SMALL;
+    int32_t* table = nullptr;
+    if (bf1::noalloc_scratch(&table) != hipSuccess) return BF1_ERR_HIP;
+    int32_t* row_ptr = table;
+    int32_t* col_idx = table + (NB + 1);
+    hipStream_t s = (hipStream_t)stream;
+    // The planner rewrites every entry the attention kernel reads, so nothing
+    // left in the scratch by an earlier call matters.
+    if (bf1::launch_plan((int32_t)NB, L, row_ptr, col_idx, s) != hipSuccess) return BF1_ERR_HIP;
+    bf1::AttnArgs a{Q, K, V, O, LSE, row_ptr, col_idx, nnz, batch, n, Hq, Hkv, head_dim, B, false};
+    return run_attn(a, s);
+}
+
 int bf1_attn_fwd_csr(const void* Q, const void* K, const void* V, void* O, float* LSE,
                      int32_t batch, int64_t n, int32_t Hq, int32_t Hkv, int32_t head_dim,
                      int32_t B, const int32_t* row_ptr, const int32_t* col_idx, int64_t nnz,

@@ -99,6 +99,12 @@ struct DecodeArgs {
 };
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
 
+// Fixed device scratch of the forward that allocates nothing: capacity in
+// int32 entries (row_ptr and col_idx of one route table), and the address of
+// the current device's copy (looked up once per device, then cached).
+constexpr int64_t kNoallocInts = int64_t(1) << 20;  // 4 MiB
+hipError_t noalloc_scratch(int32_t** ptr);
+
 // Route planner: row_ptr[0..NB], col_idx[0..nnz) on `stream`.
 hipError_t launch_plan(int32_t NB, int32_t L, int32_t* row_ptr, int32_t* col_idx,
                        hipStream_t stream);

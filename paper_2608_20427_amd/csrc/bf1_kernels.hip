@@ -29,6 +29,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <map>
+#include <mutex>
 #include <type_traits>
 
 #include "bf1_device.h"
@@ -599,7 +601,37 @@ hipError_t dispatch_g(const AttnArgs& a, hipStream_t s) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Fixed scratch of the forward that allocates nothing
+// ---------------------------------------------------------------------------
+// The route table of bf1_attn_fwd_noalloc (row_ptr, then col_idx right after
+// it) lives in this array; each device holds its own copy for the life of the
+// process.  In host code the name is a stand-in for the symbol, never a
+// device address: the address of a device's copy comes from
+// hipGetSymbolAddress, taken once per device with that device current, and
+// only that address is handed to kernels.
+static __device__ __align__(256) int32_t scratch[kNoallocInts];
+
 }  // namespace
+
+hipError_t noalloc_scratch(int32_t** ptr) {
+    static std::mutex mu;
+    static std::map<int, int32_t*> addr;  // device -> address of its copy
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = addr.find(dev);
+    if (it == addr.end()) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        it = addr.emplace(dev, static_cast<int32_t*>(p)).first;
+    }
+    *ptr = it->second;
+    return hipSuccess;
+}
 
 hipError_t launch_plan(int32_t NB, int32_t L, int32_t* row_ptr, int32_t* col_idx,
                        hipStream_t stream) {

@@ -133,6 +133,7 @@ static void runtime_errors_map_to_bf1_err_hip() {
     int32_t* ip = reinterpret_cast<int32_t*>(P);
     CHECK(bf1_plan(4096, 64, 2, ip, ip, 1 << 20, nullptr) == BF1_ERR_HIP);
     CHECK(bf1_attn_fwd(P, P, P, P, PF, 1, 4096, 16, 8, 128, 64, 2, nullptr) == BF1_ERR_HIP);
+    CHECK(bf1_attn_fwd_noalloc(P, P, P, P, PF, 1, 4096, 16, 8, 128, 64, 2, nullptr) == BF1_ERR_HIP);
     CHECK(bf1_attn_fwd_csr(P, P, P, P, PF, 1, 4096, 16, 8, 128, 64, ip, ip, 442, nullptr) == BF1_ERR_HIP);
     CHECK(bf1_dense_causal_fwd(P, P, P, P, PF, 1, 4096, 16, 8, 128, nullptr) == BF1_ERR_HIP);
     CHECK(bf1_attn_bwd(P, P, P, P, P, PF, PF, PF, PF, 1, 4096, 16, 8, 128, 64, 2, P, int64_t(1) << 40,
@@ -170,6 +171,13 @@ static void plan_cache_and_capture() {
     CHECK(bf1_attn_bwd(P, P, P, P, P, PF, PF, PF, PF, 1, 30001, 16, 8, 128, 64, 2, P, int64_t(1) << 40,
                        nullptr) == BF1_OK);
     CHECK(g_stub.bwds == 2);
+    // the forward that allocates nothing: no allocation, and an oversized
+    // table is refused before any call
+    const long m1 = g_stub.mallocs;
+    CHECK(bf1_attn_fwd_noalloc(P, P, P, P, PF, 2, 30001, 16, 8, 128, 64, 2, nullptr) == BF1_OK);
+    CHECK(bf1_attn_fwd_noalloc(P, P, P, P, PF, 1, int64_t(1) << 23, 2, 1, 128, 64, 2, nullptr) ==
+          BF1_ERR_BUFFER_TOO_SMALL);
+    CHECK(g_stub.mallocs == m1);
     bf1_release_plans();
     CHECK(g_stub.mallocs == g_stub.frees);
     std::printf("allocations %ld frees %ld\n", g_stub.mallocs, g_stub.frees);

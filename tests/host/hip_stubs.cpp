@@ -82,4 +82,10 @@ hipError_t launch_decode_plan(const DecodePlanArgs&, hipStream_t) {
 hipError_t launch_decode(const DecodeArgs&, hipStream_t) {
     return g_stub.fail ? hipErrorLaunchFailure : hipSuccess;
 }
+hipError_t noalloc_scratch(int32_t** ptr) {
+    if (g_stub.fail) return hipErrorInvalidSymbol;
+    static int32_t table[kNoallocInts];
+    *ptr = table;
+    return hipSuccess;
+}
 }  // namespace bf1
