@@ -43,7 +43,18 @@ The last line of stdout is one JSON record:
              weights (§4.3, §5.3): warm time to first token at 8K / 16K / 32K
              with every attention layer dense, the middle eight on the BF1
              route, and all 28 on the BF1 route (timing only)
+  sweep      the length sweep n = 1K..64K for block widths 64 and 128 (the
+             metric's range): BF1 and the in-house dense kernel per point,
+             timed two ways with the two-order protocol -- calls captured in a
+             HIP graph and replayed (no host launch cost, which dominates
+             short lengths, but graph nodes add a few microseconds between
+             kernels) and events around each host call (kernel time plus any
+             launch gap).  Both bound the kernel's device time from above;
+             device_ms is the smaller.  % of the bf16 MFMA peak and the
+             BF1/dense speedup follow from device_ms.
   cpu_baseline  the fp64 CPU oracle on a bounded sample of the workload
+  cpu_baseline_configs  the same oracle on the tiny (n=512), n=4096 and
+             n=30001 batch-2 peaked workloads
 
 --sweep additionally times n = 1K..64K for block widths 64 and 128 with the
 two-order protocol and writes one JSON record per point to --sweep-out.
@@ -82,6 +93,8 @@ def parse():
     ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-ttft", action="store_true")
+    ap.add_argument("--no-sweep-device", action="store_true",
+                    help="skip the default 1K-64K device-time sweep")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time bound of the CPU oracle sample")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
@@ -222,6 +235,79 @@ def run_point(torch, bf1, w, q, k, v, warmup, reps, with_dense=True):
                         "speedup_vs_sdpa": ss["ms"] / sb["ms"]})
             del f_sdpa
     return rec
+
+
+def graph_reps(torch, fn, inner, reps):
+    """Device time per call of fn (ms, one value per replay): `inner` calls
+    captured in one HIP graph on a side stream, the graph replayed `reps`
+    times with events around each replay."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(inner):
+            fn()
+    g.replay()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in ev:
+        a.record()
+        g.replay()
+        b.record()
+    torch.cuda.synchronize()
+    out = [a.elapsed_time(b) / inner for a, b in ev]
+    del g
+    return out
+
+
+def sweep_device(torch, bf1, synth, reps=8):
+    """The 1K..64K sweep for b = 64 and 128: per point BF1 and dense device
+    time (graph replay) and per-call time, each in both orders (median of the
+    two order medians)."""
+    out = []
+    for w64, w128 in zip(synth.sweep(64), synth.sweep(128)):
+        q, k, v = synth.make_qkv(w64, device="cuda")     # the two sweeps share inputs (same seed)
+        o = torch.empty_like(q)
+        lse = torch.empty((1, w64.Hq, w64.n), dtype=torch.float32, device="cuda")
+        f_dense = lambda: bf1.dense_causal_fwd(q, k, v, out=o, lse=lse)
+        dense_flops = 4 * w64.d * (w64.n * (w64.n + 1) // 2) * w64.Hq * w64.batch
+        for w in (w64, w128):
+            rp, ci = bf1.plan(w.n, w.b, w.L)
+            f_bf1 = lambda: bf1.attn_fwd_csr(q, k, v, w.b, rp, ci, out=o, lse=lse)
+            flops = bf1.selected_flops(w.batch, w.n, w.Hq, w.d, w.b, w.L)
+            inner_d = max(1, min(16, (1 << 16) // w.n * 2))
+            a1 = graph_reps(torch, f_bf1, 16, reps)
+            d1 = graph_reps(torch, f_dense, inner_d, reps)
+            d2 = graph_reps(torch, f_dense, inner_d, reps)
+            a2 = graph_reps(torch, f_bf1, 16, reps)
+            med = lambda x, y: statistics.median([statistics.median(x), statistics.median(y)])
+            gb, gd = med(a1, a2), med(d1, d2)
+            cb, cd = two_order(torch, f_bf1, f_dense, 3, 10)
+            bd, dd = min(gb, cb["ms"]), min(gd, cd["ms"])
+            plan_ms = statistics.median(graph_reps(torch, lambda: bf1.plan(w.n, w.b, w.L, rp, ci), 16, 4))
+            rec = {"n": w.n, "b": w.b, "L": w.L, "Hq": w.Hq, "Hkv": w.Hkv, "head_dim": w.d, "seed": w.seed,
+                   "selected_gflop": flops / 1e9, "dense_gflop": dense_flops / 1e9,
+                   "bf1_device_ms": bd, "bf1_device_tflops": flops / bd / 1e9,
+                   "bf1_device_pct_peak": 100 * flops / bd / 1e9 / PEAK_BF16_TFLOPS,
+                   "dense_device_ms": dd, "dense_device_tflops": dense_flops / dd / 1e9,
+                   "dense_device_pct_peak": 100 * dense_flops / dd / 1e9 / PEAK_BF16_TFLOPS,
+                   "speedup_device": dd / bd,
+                   "bf1_graph_ms": gb, "dense_graph_ms": gd,
+                   "bf1_call_ms": cb["ms"], "dense_call_ms": cd["ms"], "speedup_call": cd["ms"] / cb["ms"],
+                   "plan_device_us": plan_ms * 1e3, "pair_reduction": dense_flops / flops}
+            out.append(rec)
+            log(f"sweep n={w.n} b={w.b}: bf1 {bd * 1e3:.1f} us device ({rec['bf1_device_pct_peak']:.1f}% of peak;"
+                f" graph {gb * 1e3:.1f}, per call {cb['ms'] * 1e3:.1f}); dense {dd * 1e3:.1f} us device "
+                f"({rec['dense_device_pct_peak']:.1f}%); speedup {dd / bd:.2f}x device, "
+                f"{cd['ms'] / cb['ms']:.2f}x per call; plan {plan_ms * 1e3:.1f} us")
+            del rp, ci
+        del q, k, v, o, lse
+        torch.cuda.empty_cache()
+    return out
 
 
 def backward_point(torch, bf1, synth, w, q, k, v, warmup, reps):
@@ -502,6 +588,9 @@ def main():
             f" speedup {point.get('speedup_vs_dense', 0):.2f}x; PyTorch SDPA {point.get('sdpa_ms', 0):.4f} ms,"
             f" speedup {point.get('speedup_vs_sdpa', 0):.2f}x")
 
+    if not args.no_sweep_device:
+        rec["sweep"] = sweep_device(torch, bf1, synth)
+
     if not args.no_backward:
         bp = backward_point(torch, bf1, synth, w, q, k, v, args.warmup, args.reps)
         rec["backward"] = bp
@@ -555,6 +644,13 @@ def main():
         rec["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
         log(f"cpu baseline {rec['cpu_baseline']['value'] * 1e3:.3f} GFLOP/s in "
             f"{rec['cpu_baseline']['seconds']:.1f} s")
+        rec["cpu_baseline_configs"] = []
+        for name in ("tiny_n512", "qwen_n4096", "qwen_n30001_b2_peaked"):
+            cb = cpu_baseline(synth.WORKLOADS[name], 10.0)
+            cb["workload"] = name
+            rec["cpu_baseline_configs"].append(cb)
+            log(f"cpu baseline {name}: {cb['value'] * 1e3:.3f} GFLOP/s, {cb['gflop']:.2f} GFLOP in "
+                f"{cb['seconds']:.1f} s")
     print(json.dumps(rec), flush=True)
 
 
