@@ -301,6 +301,24 @@ int bf1_decode_attn(const void* Q, const void* K_pages, const void* V_pages, con
                     int32_t batch, int32_t Hq, int32_t Hkv, int32_t head_dim, int32_t B,
                     void* workspace, int64_t workspace_bytes, void* stream);
 
+/*
+ * Key split of the forward kernels (bf1_attn_fwd, bf1_attn_fwd_noalloc,
+ * bf1_attn_fwd_csr, bf1_dense_causal_fwd), process-wide:
+ *   0  automatic (the default): when a launch has at most one work item (one
+ *      query block of one kv-head, all its q-heads) per compute unit and its
+ *      routes average at least 8 key tiles of 64 keys per item, each
+ *      workgroup runs two groups of waves that take alternate key tiles of
+ *      the route and merge their partial softmax states at the end, halving
+ *      the chain of tiles per workgroup (in practice: the dense comparator
+ *      below ~4K tokens; BF1 routes are too short to gain).  The result is the
+ *      same attention (§3.1) up to the order of the fp32 sums.
+ *   1  never split;   2  always split.
+ * Each setting is deterministic; the two paths agree within the parity
+ * bars, not bitwise.  Intended for tuning and tests; calls in flight are not
+ * affected.  Returns BF1_ERR_INVALID_ARG for any other mode.
+ */
+int bf1_set_forward_key_split(int32_t mode);
+
 /* Frees every cached plan (device memory owned by the library).  Must not
  * race with in-flight bf1_attn_fwd / bf1_attn_bwd calls that use those plans. */
 void bf1_release_plans(void);

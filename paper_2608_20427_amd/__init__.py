@@ -19,6 +19,7 @@ __all__ = [
     "BF1Error", "lib_path", "load", "version", "status_string", "plan_size", "plan",
     "attn_fwd", "attn_fwd_csr", "dense_causal_fwd", "release_plans", "selected_flops",
     "plan_transposed", "bwd_workspace_size", "attn_bwd", "selected_bwd_flops", "attn_fwd_noalloc",
+    "set_forward_key_split",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -72,6 +73,8 @@ def load():
     lib.bf1_attn_fwd_csr.argtypes = attn + [i32, vp, vp, i64, vp]
     lib.bf1_dense_causal_fwd.restype = ctypes.c_int
     lib.bf1_dense_causal_fwd.argtypes = attn + [vp]
+    lib.bf1_set_forward_key_split.restype = ctypes.c_int
+    lib.bf1_set_forward_key_split.argtypes = [i32]
     lib.bf1_release_plans.restype = None
     lib.bf1_release_plans.argtypes = []
     lib.bf1_plan_transposed.restype = ctypes.c_int
@@ -277,6 +280,11 @@ def dense_causal_fwd(q, k, v, out=None, lse=None, want_lse=True, stream=None):
 
 def release_plans():
     load().bf1_release_plans()
+
+
+def set_forward_key_split(mode):
+    """Forward key split: 0 automatic (default), 1 never, 2 always."""
+    _check(load().bf1_set_forward_key_split(int(mode)), "bf1_set_forward_key_split")
 
 
 def plan_transposed(n, B=64, L=2):

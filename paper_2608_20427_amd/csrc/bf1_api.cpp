@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <array>
+#include <atomic>
 #include <map>
 #include <mutex>
 #include <tuple>
@@ -44,6 +45,9 @@ std::map<std::tuple<int, int64_t, int32_t, int32_t>, Plan> g_plans;
 std::map<int, hipStream_t> g_plan_streams;  // per device, created on first use
 
 int status_of(hipError_t e) { return e == hipSuccess ? BF1_OK : BF1_ERR_HIP; }
+
+// Forward key split (bf1_set_forward_key_split): 0 automatic, 1 never, 2 always.
+std::atomic<int> g_key_split{0};
 
 // True (and BF1_OK) if `s` is being captured into a graph.
 int capturing(hipStream_t s, bool* yes) {
@@ -108,7 +112,10 @@ int64_t decode_ws_bytes(int64_t batch, int64_t Hq, int64_t Hkv, int64_t D, int64
     return (b + 255) / 256 * 256;
 }
 
-int run_attn(const bf1::AttnArgs& a, hipStream_t s) { return status_of(bf1::launch_attention(a, s)); }
+int run_attn(bf1::AttnArgs a, hipStream_t s) {
+    a.key_split = g_key_split.load(std::memory_order_relaxed);
+    return status_of(bf1::launch_attention(a, s));
+}
 
 // Cached forward route of (current device, n, B, L), built by the planner
 // kernel on first use and complete on return.  `s` is the caller's stream
@@ -530,6 +537,12 @@ int bf1_attn_bwd(const void* Q, const void* K, const void* V, const void* O, con
                    plan.row_ptr, plan.col_idx, plan.nnz, bp.users, bp.uoffs, bp.nusers, bp.segs, bp.nseg,
                    bp.reds, bp.nred, bp.nslots, batch, n, Hq, Hkv, B, head_dim, L};
     return status_of(bf1::launch_backward(a, s));
+}
+
+int bf1_set_forward_key_split(int32_t mode) {
+    if (mode < 0 || mode > 2) return BF1_ERR_INVALID_ARG;
+    g_key_split.store(mode, std::memory_order_relaxed);
+    return BF1_OK;
 }
 
 void bf1_release_plans(void) {

@@ -22,6 +22,7 @@ struct AttnArgs {
     int32_t head_dim;       // 64 or 128
     int32_t B;              // block width 64 or 128 (BF1 route)
     bool dense;             // implicit route {0..j} over 64-token blocks
+    int32_t key_split = 0;  // 0 automatic, 1 one key group, 2 two key groups per workgroup
 };
 
 // Backward (head_dim 64 or 128; G * B >= 128).  All pointers are device memory.

@@ -146,8 +146,15 @@ __device__ __forceinline__ void lds_read_tr16_x8(uint32_t addr, u32x2 (&v)[8]) {
 // Attention forward
 // ---------------------------------------------------------------------------
 
-template <int D, int G, int BW, int NW, bool DENSE>
-__global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
+// KSPLIT = 2 (short sequences, at most one work item per compute unit): the
+// workgroup holds two groups of NW waves that cover the same query rows and
+// walk alternate tiles of the route (group 0 the even positions, group 1 the
+// odd ones), each with its own LDS tiles; group 1 hands its running max, sums
+// and unnormalised rows to group 0 through LDS, which merges and stores.  An
+// item's chain of key tiles is halved, and two waves share each SIMD where a
+// single workgroup would otherwise leave one.
+template <int D, int G, int BW, int NW, bool DENSE, int KSPLIT>
+__global__ __launch_bounds__(NW * 64 * KSPLIT, KSPLIT == 1 ? 2 : 1) void attn_fwd_kernel(
     const __bf16* __restrict__ Q, const __bf16* __restrict__ K, const __bf16* __restrict__ V,
     __bf16* __restrict__ O, float* __restrict__ LSE, const int32_t* __restrict__ row_ptr,
     const int32_t* __restrict__ col_idx, int64_t nnz, int32_t n, int32_t NB, int32_t batch_hkv,
@@ -164,12 +171,16 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     constexpr int SEG_PER_WAVE = SEGS / NW;
     static_assert(ROWS * NCHUNK == G * BW, "rows must tile the stacked group");
     static_assert(SEGS % NW == 0, "segments must split over the waves");
+    static_assert(KSPLIT == 1 || KSPLIT == 2, "one or two key groups");
 
-    __shared__ TileSmem<D> sm;
+    __shared__ TileSmem<D> smem[KSPLIT];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+    const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+    const int grp = wid / NW;     // key group (0 unless KSPLIT = 2)
+    const int wave = wid % NW;    // wave within its group
+    TileSmem<D>& sm = smem[grp];
     const int col = lane & 31;   // query column owned by this lane
     const int half = lane >> 5;  // lane half: selects k-range / row group
 
@@ -245,6 +256,25 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
             advance();
         }
         return false;
+    };
+    // This group's next tile.  With two key groups the route's tiles are
+    // taken in pairs: a pair exists if its first tile does (both groups see
+    // the same walk, so they agree on the number of steps), and the group
+    // whose tile of the pair is missing runs that step on a dummy tile whose
+    // scores are all masked (it contributes exactly nothing).
+    auto next_own = [&](int32_t& ti, int& tu, bool& real) -> bool {
+        if (KSPLIT == 1) {
+            real = next_tile(ti, tu);
+            return real;
+        }
+        int32_t t0 = 0, t1 = 0;
+        int u0 = 0, u1 = 0;
+        if (!next_tile(t0, u0)) return false;
+        const bool has1 = next_tile(t1, u1);
+        ti = grp == 0 ? t0 : t1;
+        tu = grp == 0 ? u0 : u1;
+        real = grp == 0 || has1;
+        return true;
     };
 
     // ---- direct buffer -> LDS staging ----------------------------------------
@@ -325,10 +355,11 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     // ---- prologue: K0, V0 and K1 resident, S0 computed ----------------------
     int32_t ti0 = 0, ti1 = 0, ti2 = 0;
     int tu0 = 0, tu1 = 0, tu2 = 0;
-    if (!next_tile(ti0, tu0)) {
+    bool rl0 = true, rl1 = true, rl2 = true;  // tile k, k+1, k+2 is real (not a dummy)
+    if (!next_own(ti0, tu0, rl0)) {
         // A row with no usable key block (possible only for a caller route
         // table): O = 0, LSE = -inf.
-        if (qvalid) {
+        if (qvalid && grp == 0) {
             __bf16* Orow = O + (((int64_t)beta * Hq + head) * (int64_t)n + qpos) * D;
 #pragma unroll
             for (int c = 0; c < D / 2; c += 8)
@@ -338,10 +369,10 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
         }
         return;
     }
-    bool h1 = next_tile(ti1, tu1);
-    load_k(0, tile_off(true, ti0, tu0));
-    load_v(0, tile_off(true, ti0, tu0));
-    if (h1) load_k(1, tile_off(true, ti1, tu1));
+    bool h1 = next_own(ti1, tu1, rl1);
+    load_k(0, tile_off(rl0, ti0, tu0));
+    load_v(0, tile_off(rl0, ti0, tu0));
+    if (h1) load_k(1, tile_off(rl1, ti1, tu1));
     __builtin_amdgcn_s_waitcnt(VMCNT0);
     __syncthreads();
 
@@ -354,8 +385,13 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     // The decision is per row (per lane), so a row's arithmetic never depends
     // on other rows' data; the wave only skips the rescale work when no row
     // needs it (alpha = 1 exactly for the others).
-    auto tile_stats = [&](f32x16 (&sc)[2], int32_t ti, int tu, float& m_cand) -> bool {
-        if (ti == j) {  // self block: token-level causal triangle
+    auto tile_stats = [&](f32x16 (&sc)[2], int32_t ti, int tu, bool real, float& m_cand) -> bool {
+        if (KSPLIT > 1 && !real) {  // dummy tile: every score masked
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) sc[kt][r] = -INFINITY;
+        } else if (ti == j) {  // self block: token-level causal triangle
             const int kin = tu * KT, qin = p0 + col;
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt)
@@ -393,8 +429,9 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     score_mfma(std::integral_constant<int, 0>{}, s_a);
     {
         float mc;
-        const bool nd = tile_stats(s_a, ti0, tu0, mc);
-        apply_rescale(nd, mc);
+        // acc and the sums are still zero: the first tile only sets the
+        // running max (the rescale would multiply zeros)
+        if (tile_stats(s_a, ti0, tu0, rl0, mc)) m_run = mc;
     }
 
     // ---- steady state --------------------------------------------------------
@@ -410,11 +447,12 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     // LDS read below is a lane-constant base plus an immediate offset).
     auto step = [&](auto par_c, f32x16 (&s_cur)[2], f32x16 (&s_nxt)[2]) -> bool {
         constexpr int PAR = decltype(par_c)::value;
-        const bool h2 = h1 && next_tile(ti2, tu2);
+        const bool h2 = h1 && next_own(ti2, tu2, rl2);
         // The loads of K_k+2 and V_k+1 are spread over phase 1; a tile that
-        // does not exist reads zeros past the end of the head (no traffic).
-        const uint32_t soff_k2 = tile_off(h2, ti2, tu2);
-        const uint32_t soff_v1 = tile_off(h1, ti1, tu1);
+        // does not exist (or a dummy) reads zeros past the end of the head
+        // (no traffic).
+        const uint32_t soff_k2 = tile_off(h2 && rl2, ti2, tu2);
+        const uint32_t soff_v1 = tile_off(h1 && rl1, ti1, tu1);
 
         // phase 1: scores of tile k+1 (unused after the last tile), P of tile
         // k.  Step q issues score MFMA q, prefetches the K operand of MFMA q+KPF
@@ -502,7 +540,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
                 acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w),
                                                                   pb[t], acc[dt], 0, 0, 0);
             }
-            if (dt == 0 && h1) need = tile_stats(s_nxt, ti1, tu1, m_cand);
+            if (dt == 0 && h1) need = tile_stats(s_nxt, ti1, tu1, rl1, m_cand);
         }
         if (h1) apply_rescale(need, m_cand);
 
@@ -511,8 +549,10 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
         if (!h1) return false;
         ti0 = ti1;
         tu0 = tu1;
+        rl0 = rl1;
         ti1 = ti2;
         tu1 = tu2;
+        rl1 = rl2;
         h1 = h2;
         return true;
     };
@@ -536,6 +576,43 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
     // tiles before this; no other wave touches this slice.  The stores are
     // non-temporal: O is not read again here, and streaming it through L2
     // evicted K/V tiles that other workgroups were still reusing.
+    if (KSPLIT > 1) {
+        // Group 1 hands (m, l, l_bf, acc) of its lanes to group 0 through its
+        // own (now idle) tiles and group 0's V tiles; wave w of group 1 holds
+        // the same query rows, lane for lane, as wave w of group 0.  The last
+        // step's barrier ordered every tile read before this.
+        float* accx = reinterpret_cast<float*>(&smem[KSPLIT - 1]) + wave * (DT * 16 * 64);
+        float* stx = reinterpret_cast<float*>(&smem[0].v[0][0]) + wave * (3 * 64);
+        if (grp == 1) {
+#pragma unroll
+            for (int t = 0; t < DT; ++t)
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4) {
+                    const f32x4 v4 = {acc[t][4 * r4], acc[t][4 * r4 + 1], acc[t][4 * r4 + 2],
+                                      acc[t][4 * r4 + 3]};
+                    *reinterpret_cast<f32x4*>(accx + ((t * 4 + r4) * 64 + lane) * 4) = v4;
+                }
+            stx[lane] = m_run;
+            stx[64 + lane] = l_run;
+            stx[128 + lane] = l_bf;
+        }
+        __syncthreads();
+        if (grp == 1) return;
+        const float m1 = stx[lane], l1 = stx[64 + lane], lb1 = stx[128 + lane];
+        const float m = __builtin_elementwise_maximum(m_run, m1);
+        const float a0 = __builtin_amdgcn_exp2f(m_run - m), a1 = __builtin_amdgcn_exp2f(m1 - m);
+#pragma unroll
+        for (int t = 0; t < DT; ++t)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+                const f32x4 v4 = *reinterpret_cast<const f32x4*>(accx + ((t * 4 + r4) * 64 + lane) * 4);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) acc[t][4 * r4 + c] = fmaf(acc[t][4 * r4 + c], a0, v4[c] * a1);
+            }
+        l_run = fmaf(l_run, a0, l1 * a1);
+        l_bf = fmaf(l_bf, a0, lb1 * a1);
+        m_run = m;
+    }
     const float l_tot = pair_sum(l_run);
     const float inv = 1.f / pair_sum(l_bf);
     constexpr int OCH = D / 8;                 // 16-byte chunks per row
@@ -567,6 +644,34 @@ __global__ __launch_bounds__(NW * 64, 2) void attn_fwd_kernel(
         LSE[((int64_t)beta * Hq + head) * (int64_t)n + qpos] = (m_run + log2f(l_tot)) * LN2;
 }
 
+// Two key groups per workgroup: never (mode 1), always (mode 2), or (mode 0,
+// automatic) when the launch has at most one work item per compute unit and
+// its routes average at least 8 key tiles per item.  Measured on MI355X: the
+// dense comparator gains 4-11% at 1K-4K tokens, while BF1 routes at those
+// lengths (3-7 tiles per item) lose 0-11%, their time being set by fixed
+// per-item latencies rather than by the chain of tiles.
+bool use_key_split(int mode, int64_t items, int64_t tiles) {
+    if (mode == 1) return false;
+    if (mode == 2) return true;
+    if (tiles < 8 * items) return false;
+    static std::mutex mu;
+    static std::map<int, int> cus;  // device -> compute units
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return false;
+    int cu = 0;
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        auto it = cus.find(dev);
+        if (it == cus.end()) {
+            if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cu = 0;
+            cus.emplace(dev, cu);
+        } else {
+            cu = it->second;
+        }
+    }
+    return cu > 0 && items <= cu;
+}
+
 template <int D, int G, int BW, bool DENSE>
 hipError_t launch_attn(const AttnArgs& a, hipStream_t stream) {
     constexpr int NW = (G * BW) >= 128 ? 4 : (G * BW) / 32;
@@ -577,10 +682,21 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t stream) {
     if (items == 0) return hipSuccess;
     if (items > 0x7fffffff) return hipErrorInvalidValue;
     const float c_log2 = (1.0f / sqrtf((float)D)) * LOG2E;
-    hipLaunchKernelGGL((attn_fwd_kernel<D, G, BW, NW, DENSE>), dim3((unsigned)items), dim3(NW * 64),
-                       0, stream, (const __bf16*)a.Q, (const __bf16*)a.K, (const __bf16*)a.V,
-                       (__bf16*)a.O, a.LSE, a.row_ptr, a.col_idx, a.nnz, (int32_t)a.n, NB,
-                       a.batch * a.Hkv, a.Hkv, c_log2);
+    // key tiles the launch walks (the dense route {0..j} has NB (NB + 1) / 2
+    // blocks per kv-head; a caller table is taken at its size)
+    const int64_t blocks = DENSE ? (int64_t)NB * (NB + 1) / 2 : a.nnz;
+    const int64_t tiles = blocks * (BW / KT) * a.batch * a.Hkv * NCHUNK;
+    if (use_key_split(a.key_split, items, tiles)) {
+        hipLaunchKernelGGL((attn_fwd_kernel<D, G, BW, NW, DENSE, 2>), dim3((unsigned)items),
+                           dim3(2 * NW * 64), 0, stream, (const __bf16*)a.Q, (const __bf16*)a.K,
+                           (const __bf16*)a.V, (__bf16*)a.O, a.LSE, a.row_ptr, a.col_idx, a.nnz,
+                           (int32_t)a.n, NB, a.batch * a.Hkv, a.Hkv, c_log2);
+    } else {
+        hipLaunchKernelGGL((attn_fwd_kernel<D, G, BW, NW, DENSE, 1>), dim3((unsigned)items),
+                           dim3(NW * 64), 0, stream, (const __bf16*)a.Q, (const __bf16*)a.K,
+                           (const __bf16*)a.V, (__bf16*)a.O, a.LSE, a.row_ptr, a.col_idx, a.nnz,
+                           (int32_t)a.n, NB, a.batch * a.Hkv, a.Hkv, c_log2);
+    }
     return hipGetLastError();
 }
 

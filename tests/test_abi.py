@@ -303,3 +303,10 @@ def test_decode_invalid_arguments_rejected_without_device(lib):
     assert attn(ws=None) == bf1.BF1_ERR_INVALID_ARG
     assert attn(ws=ctypes.c_void_p((1 << 20) + 8)) == bf1.BF1_ERR_INVALID_ARG
     assert attn(wsb=1024) == bf1.BF1_ERR_BUFFER_TOO_SMALL
+
+
+def test_key_split_mode_checked(lib):
+    assert lib.bf1_set_forward_key_split(3) == bf1.BF1_ERR_INVALID_ARG
+    assert lib.bf1_set_forward_key_split(-1) == bf1.BF1_ERR_INVALID_ARG
+    for mode in (1, 2, 0):
+        assert lib.bf1_set_forward_key_split(mode) == bf1.BF1_OK
