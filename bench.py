@@ -567,7 +567,7 @@ def main():
         "pct_mfma_peak": 100 * achieved / PEAK_BF16_TFLOPS,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
-                     "kernel": "attn_fwd_kernel<128,2,64,4,false>",
+                     "kernel": "attn_fwd_kernel<128,2,64,4,false,1>",
                      "kernel_ms": attn_ms},
     }
 
