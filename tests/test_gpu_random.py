@@ -1,14 +1,16 @@
-"""Seeded random configurations of the forward (both key-group paths) and the
-backward, compared with the fp64 oracle on the GPU.
+"""Seeded random configurations of the forward (both key-group paths), the
+backward and the paged decode, compared with the fp64 oracle on the GPU.
 
 The fixed grids elsewhere pin every advertised (head_dim, group, block width)
 instance at one ragged length and L = 2; here the other dimensions vary
 together: batch 1-3, 1 to 1800 tokens (partial last blocks, n below one
 block, exact multiples of the block), local width L 0-5 (§3.1 fixes L = 2 for
 the reported configuration; other widths follow the reading stated with the
-oracle's route), 1-3 kv-heads.  Bars: the forward's (O max-abs 2e-2,
-mean-abs 2e-3, LSE max-abs 1e-3) and the backward's element-wise bound
-derived from its arithmetic (test_gpu_backward.py).
+oracle's route), 1-3 kv-heads; decode batches mix sequence lengths (one
+token, block edges, ragged) over a shuffled page pool with NaN decoy pages.
+Bars: the forward's (O max-abs 2e-2, mean-abs 2e-3, LSE max-abs 1e-3, which
+decode shares) and the backward's element-wise bound derived from its
+arithmetic (test_gpu_backward.py).
 """
 
 import numpy as np
@@ -17,6 +19,7 @@ import torch
 
 import paper_2608_20427_amd as bf1
 import test_gpu_backward as TB
+import test_gpu_decode as TD
 import test_gpu_parity as TP
 from oracle import bf1_oracle as orc
 from paper_2608_20427_amd import synth
@@ -48,7 +51,33 @@ def _configs(count, seed):
     return out
 
 
+def _decode_configs(count, seed):
+    """(batch, Hq, Hkv, d, B, L, dense, seq_lens) drawn from a fixed generator."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(count):
+        d = int(rng.choice([64, 128]))
+        B = int(rng.choice([64, 128]))
+        G = int(rng.choice([1, 2, 4, 8]))
+        Hkv = int(rng.integers(1, 4))
+        batch = int(rng.integers(1, 13))
+        L = int(rng.integers(0, 6))
+        dense = bool(rng.random() < 0.2)
+        lens = []
+        for _ in range(batch):
+            kind = int(rng.integers(0, 4))
+            if kind == 0:
+                lens.append(1)
+            elif kind == 1:
+                lens.append(B * int(rng.integers(1, 40)) + int(rng.choice([-1, 0, 1])))
+            else:
+                lens.append(int(rng.integers(2, 5000)))
+        out.append((batch, G * Hkv, Hkv, d, B, L, dense, [max(1, x) for x in lens]))
+    return out
+
+
 FWD = _configs(24, 20260)
+DEC = _decode_configs(12, 20262)
 BWD = [c for c in _configs(40, 20261) if (c[2] // c[3]) * c[5] >= 128][:12]
 ident = lambda c: "x".join(map(str, c))
 
@@ -88,3 +117,17 @@ def test_backward_random(cfg):
     (dq, dk, dv), ref, terms = TB.run_case(w)
     for name, got, r, t in zip(("dQ", "dK", "dV"), (dq, dk, dv), ref, terms):
         TB.check_bound(got, r, t, tag=f"random {cfg} {name}")
+
+
+@pytest.mark.parametrize("cfg", DEC, ids=lambda c: "x".join(map(str, c[:7])))
+def test_decode_random(cfg):
+    batch, Hq, Hkv, d, B, L, dense, lens = cfg
+    TP.say(f"random decode {cfg[:7]} lens {lens}")
+    w = synth.DecodeWorkload("rand", batch, max(lens), Hq, Hkv, d, B, L, seed=1300 + sum(lens))
+    (q, k, v, sl, _), dev = TD.setup_case(w, np.array(lens, dtype=np.int32), dense=dense)
+    o, l, _ = TD.run_decode(w, dev, dense=dense)
+    # the dense plan lists every earlier block: the oracle's route with a local
+    # width that covers all of them
+    L_ref = int(max(lens)) // B + 2 if dense else L
+    o_ref, l_ref = orc.attn_decode_fp64(synth.to_f64(q), synth.to_f64(k), synth.to_f64(v), sl, B, L_ref)
+    TD.compare(o, l, o_ref, l_ref, f"random decode {cfg[:7]}")
