@@ -23,7 +23,7 @@ from dataclasses import dataclass, field, replace
 import numpy as np
 import torch
 
-__all__ = ["Workload", "WORKLOADS", "sweep", "make_qkv", "to_f64", "DecodeWorkload",
+__all__ = ["Workload", "WORKLOADS", "sweep", "make_qkv", "make_qkv_device", "to_f64", "DecodeWorkload",
            "DECODE_WORKLOADS", "decode_seq_lens", "make_decode_host", "page_cache",
            "make_decode_device", "ModelConfig", "QWEN3_06B", "make_model_weights", "make_tokens"]
 
@@ -94,6 +94,20 @@ def make_qkv(w, device="cpu"):
     if device != "cpu":
         tq, tk, tv = tq.to(device), tk.to(device), tv.to(device)
     return tq, tk, tv
+
+
+def make_qkv_device(w, device="cuda"):
+    """Q, K, V of workload w drawn on the device by a seeded torch generator
+    (for lengths whose float32 host draws would not fit in host memory):
+    bf16 standard normals in [batch, heads, n, head_dim] order, Q then K then
+    V.  Not bit-identical to make_qkv; a test gives the oracle the device's
+    bits by copying the rows it needs."""
+    g = torch.Generator(device=device)
+    g.manual_seed(w.seed)
+    q = torch.randn((w.batch, w.Hq, w.n, w.d), generator=g, device=device, dtype=torch.bfloat16)
+    k = torch.randn((w.batch, w.Hkv, w.n, w.d), generator=g, device=device, dtype=torch.bfloat16)
+    v = torch.randn((w.batch, w.Hkv, w.n, w.d), generator=g, device=device, dtype=torch.bfloat16)
+    return q, k, v
 
 
 def make_qkv_large_logits(w, q_mul=8.0, k_ramp=9.0, diag=0.0, device="cpu"):
