@@ -86,7 +86,7 @@ def parse():
     ap.add_argument("--workload", default="qwen_n32768")
     ap.add_argument("--reps", type=int, default=30, help="reps per order in the two-order protocol")
     ap.add_argument("--sweep", action="store_true")
-    ap.add_argument("--sweep-out", default=os.path.join(ROOT, "gpurun_out", "sweep.jsonl"))
+    ap.add_argument("--sweep-out", default="sweep.jsonl")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true")
@@ -625,7 +625,8 @@ def main():
                 f"all BF1 {r.get('speedup_all_vs_sdpa_dense', 0):.2f}x")
 
     if args.sweep:
-        os.makedirs(os.path.dirname(args.sweep_out), exist_ok=True)
+        if os.path.dirname(args.sweep_out):
+            os.makedirs(os.path.dirname(args.sweep_out), exist_ok=True)
         with open(args.sweep_out, "w") as f:
             for b in (64, 128):
                 for sw in synth.sweep(b):
