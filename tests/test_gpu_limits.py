@@ -1,4 +1,6 @@
-"""The longest sequence the interface accepts, n = 2^24 - 1 tokens (every
+"""Sizes at the interface's limits.
+
+The longest sequence the interface accepts, n = 2^24 - 1 tokens (every
 per-head byte offset of a head_dim 128 row then stays below 2^32), through
 the BF1 forward at head_dim 128, B = 64, L = 2, with one GQA group of two
 q-heads; the fp64 oracle checks sampled query blocks, the partial last block
@@ -11,6 +13,12 @@ side by side, with query block j as the last block.  The mask of §3.1 only
 distinguishes earlier blocks (fully visible) from the self block (causal by
 position inside the block), and both are preserved by that relabelling.
 Bars: the forward's (O max-abs 2e-2, mean-abs 2e-3, LSE max-abs 1e-3).
+
+The backward at 2^20 tokens, where its dS workspace (one 8 KB unit per
+selected block pair and q-head) passes 2^31 bytes and key block 0's list of
+16384 query blocks is cut into 1024 partial slots; sampled dQ rows and
+dK / dV rows (block 0 among them) against the oracle, with the backward's
+element-wise bound (test_gpu_backward.py).
 """
 
 import numpy as np
@@ -18,6 +26,7 @@ import pytest
 import torch
 
 import paper_2608_20427_amd as bf1
+import test_gpu_backward as TB
 import test_gpu_parity as TP
 from oracle import bf1_oracle as orc
 from paper_2608_20427_amd import synth
@@ -68,3 +77,19 @@ def test_forward_longest_supported_sequence():
     # every output row written and finite (one q-head at a time)
     for h in range(w.Hq):
         assert torch.isfinite(o[:, h]).all() and torch.isfinite(lse[:, h]).all(), h
+
+
+def test_backward_million_tokens():
+    b, L = 64, 2
+    w = synth.Workload("bwd_1m", 1, 1 << 20, 2, 1, 64, b, L, seed=20)
+    NB = orc.num_blocks(w.n, b)
+    assert bf1.bwd_workspace_size(w.batch, w.n, w.Hq, w.Hkv, w.d, b, L) > 1 << 31
+    q_blocks = [0, 1, 4097, NB - 1]
+    kv_blocks = [0, 2, 8191, NB - 1]
+    TP.say(f"backward n = {w.n}: q blocks {q_blocks}, kv blocks {kv_blocks}")
+    (dq, dk, dv), ref, terms = TB.run_case(w, q_blocks=q_blocks, kv_blocks=kv_blocks)
+    for t in (dq, dk, dv):
+        assert torch.isfinite(t).all()
+    qrows, kvrows = TB._rows(q_blocks, b, w.n), TB._rows(kv_blocks, b, w.n)
+    for name, got, r, t, rows in zip(("dQ", "dK", "dV"), (dq, dk, dv), ref, terms, (qrows, kvrows, kvrows)):
+        TB.check_bound(got, r, t, rows=rows, tag=f"n = {w.n} {name}")
