@@ -144,6 +144,18 @@ def two_order(torch, fa, fb, warmup, reps):
     return summ(a1, a2), summ(b1, b2)
 
 
+def cpu_model():
+    """The host CPU's model name (Linux /proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, max_seconds):
     """The fp64 oracle on a bounded sample of the workload: query blocks in
     an evenly spread order (heaviest first), 16 at a time, until the time
@@ -174,7 +186,7 @@ def cpu_baseline(w, max_seconds):
     flops = 4 * w.d * int(pairs) * w.Hq * w.batch
     cores = len(os.sched_getaffinity(0))
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
-            "seconds": dt, "gflop": flops / 1e9,
+            "cpu_model": cpu_model(), "seconds": dt, "gflop": flops / 1e9,
             "sample": f"{len(done)} of {NB} query blocks (strided order, heaviest first; whole "
                       f"workload if under {max_seconds:.0f} s), all {w.Hq} q-heads, batch {w.batch}, "
                       f"workload {w.name}; fp64 NumPy gathered oracle, BLAS threads = host cores"}
