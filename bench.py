@@ -16,6 +16,12 @@ The last line of stdout is one JSON record:
   roofline   the attention kernel alone: achieved TFLOP/s (HIP events on its
              stream, averaged over the K timed launches) against the
              published dense bf16 MFMA peak of MI355X (2.5 PFLOP/s)
+  mfma_reference  what a tuned library GEMM reaches on this chip: PyTorch's
+             bf16 matmul (hipBLASLt) at 8192^3 with N(0,1) operands and with
+             all-zero operands.  The chip's clock is held by its power limit,
+             and the matrix cores draw more power on random data, so the
+             sustainable bf16 rate on random operands sits well below the
+             published peak; the attention kernel's rate is given against it
   dense      the in-house dense causal kernel timed with the paper's
              protocol (5 warmups, 30 reps, two opposite orders, median of the
              two order medians, §4.3) next to BF1 timed the same way; PyTorch's
@@ -93,6 +99,7 @@ def parse():
     ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-ttft", action="store_true")
+    ap.add_argument("--no-gemm-ref", action="store_true")
     ap.add_argument("--no-sweep-device", action="store_true",
                     help="skip the default 1K-64K device-time sweep")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -205,6 +212,28 @@ def cpu_baseline(w, max_seconds, min_seconds=0.0):
             "sample": f"{what}, all {w.Hq} q-heads, batch {w.batch}, workload {w.name}; "
                       f"time bound {max_seconds:.0f} s, whole passes repeated to at least "
                       f"{min_seconds:.0f} s; fp64 NumPy gathered oracle, BLAS threads = host cores"}
+
+
+def gemm_reference(torch, achieved, N=8192):
+    """bf16 GEMM rate of the platform library (torch.matmul -> hipBLASLt) on
+    random and on all-zero operands: the matrix cores' sustainable rate on
+    random data under the chip's power limit, for reading the roofline
+    fraction (the fraction itself stays against the published peak)."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    a = torch.randn(N, N, dtype=torch.bfloat16, device="cuda", generator=g)
+    b = torch.randn(N, N, dtype=torch.bfloat16, device="cuda", generator=g)
+    z = torch.zeros_like(a)
+    c = torch.empty_like(a)
+    flops = 2.0 * N ** 3
+    out = {"what": f"torch.matmul bf16 {N}x{N}x{N} (hipBLASLt), median of 20 calls after 10 warm-up calls"}
+    for name, x, y in (("random", a, b), ("zeros", z, z)):
+        ms = statistics.median(timed_reps(torch, lambda: torch.matmul(x, y, out=c), 10, 20))
+        out[f"{name}_tflops"] = flops / (ms * 1e-3) / 1e12
+    out["random_frac_of_peak"] = out["random_tflops"] / PEAK_BF16_TFLOPS
+    out["attention_over_random_gemm"] = achieved / out["random_tflops"]
+    del a, b, z, c
+    return out
 
 
 def sdpa_fn(torch, q, k, v):
@@ -607,6 +636,13 @@ def main():
         torch.cuda.synchronize()
         log(f"calibration copy of {args.calib_copy_mb} MiB done")
         del src, dst
+
+    if not args.no_gemm_ref:
+        rec["mfma_reference"] = gemm_reference(torch, achieved)
+        mr = rec["mfma_reference"]
+        log(f"library bf16 GEMM: {mr['random_tflops']:.0f} TF/s on random operands "
+            f"({100 * mr['random_frac_of_peak']:.1f}% of peak), {mr['zeros_tflops']:.0f} TF/s on zeros; "
+            f"attention kernel at {100 * mr['attention_over_random_gemm']:.1f}% of the random-operand GEMM")
 
     if not args.no_dense:
         point = run_point(torch, bf1, w, q, k, v, args.warmup, args.reps)
