@@ -392,14 +392,15 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_kernel(
 
 // Merge of the split records of one (sequence, kv-head), in split order:
 // every thread owns one (q-head, dim) output and folds the records in groups
-// of eight (their loads issued together) into a running max / sum / row.
+// of sixteen (their loads issued together, so a selected list of up to 16
+// splits costs one load round trip) into a running max / sum / row.
 template <int D, int G, int PW>
 __global__ __launch_bounds__(DEC_THREADS) void decode_merge_kernel(
     const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ plan, int32_t stride,
     int32_t cap, __bf16* __restrict__ O, float* __restrict__ LSE, const float* __restrict__ ws,
     int32_t Hkv, int32_t nsplit, int32_t ppw) {
     constexpr int REC = G * (D + 2);
-    constexpr int U = 8;
+    constexpr int U = 16;
     const int tid = threadIdx.x;
     const int bh = blockIdx.x;
     const int h = bh % Hkv;
