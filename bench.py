@@ -64,6 +64,12 @@ The last line of stdout is one JSON record:
 
 --sweep additionally times n = 1K..64K for block widths 64 and 128 with the
 two-order protocol and writes one JSON record per point to --sweep-out.
+
+--load KIND --load-seconds S runs one workload back to back for S seconds
+and prints its time per call, nothing else (for sampling the GPU's shader
+clock from another process while it runs): attn (the BF1 forward of the
+default workload), attn_q0 (the same with Q = 0), gemm / gemm_zero (the
+8192^3 bf16 matmul of mfma_reference on N(0,1) / all-zero operands).
 """
 
 import argparse
@@ -100,6 +106,9 @@ def parse():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-ttft", action="store_true")
     ap.add_argument("--no-gemm-ref", action="store_true")
+    ap.add_argument("--load", choices=["attn", "attn_q0", "gemm", "gemm_zero"], default=None,
+                    help="run one workload back to back (see the module docstring) and exit")
+    ap.add_argument("--load-seconds", type=float, default=8.0)
     ap.add_argument("--no-sweep-device", action="store_true",
                     help="skip the default 1K-64K device-time sweep")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -234,6 +243,43 @@ def gemm_reference(torch, achieved, N=8192):
     out["attention_over_random_gemm"] = achieved / out["random_tflops"]
     del a, b, z, c
     return out
+
+
+def run_load(torch, bf1, synth, kind, seconds, workload):
+    """One workload back to back for `seconds` (the --load mode): prints the
+    number of calls and the device time per call."""
+    if kind.startswith("attn"):
+        w = synth.WORKLOADS[workload]
+        q, k, v = synth.make_qkv(w, device="cuda")
+        if kind == "attn_q0":
+            q.zero_()
+        o = torch.empty_like(q)
+        lse = torch.empty((w.batch, w.Hq, w.n), dtype=torch.float32, device="cuda")
+        rp, ci = bf1.plan(w.n, w.b, w.L)
+        fn = lambda: bf1.attn_fwd_csr(q, k, v, w.b, rp, ci, out=o, lse=lse)
+    else:
+        N = 8192
+        g = torch.Generator(device="cuda")
+        g.manual_seed(0)
+        a = torch.randn(N, N, dtype=torch.bfloat16, device="cuda", generator=g)
+        b = torch.randn(N, N, dtype=torch.bfloat16, device="cuda", generator=g)
+        if kind == "gemm_zero":
+            a.zero_()
+            b.zero_()
+        c = torch.empty_like(a)
+        fn = lambda: torch.matmul(a, b, out=c)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    calls = 0
+    t0 = time.perf_counter()
+    e0.record()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            fn()
+        calls += 20
+        torch.cuda.synchronize()
+    e1.record()
+    torch.cuda.synchronize()
+    print(f"load {kind}: {calls} calls, {e0.elapsed_time(e1) / calls * 1e3:.1f} us per call", flush=True)
 
 
 def sdpa_fn(torch, q, k, v):
@@ -544,6 +590,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     bf1.load()
+    if args.load is not None:
+        run_load(torch, bf1, synth, args.load, args.load_seconds, args.workload)
+        return
     w = synth.WORKLOADS[args.workload]
     props = torch.cuda.get_device_properties(0)
     log(f"device {props.name} CUs={props.multi_processor_count}; workload {w}")
