@@ -68,7 +68,8 @@ two-order protocol and writes one JSON record per point to --sweep-out.
 --load KIND --load-seconds S runs one workload back to back for S seconds
 and prints its time per call, nothing else (for sampling the GPU's shader
 clock from another process while it runs): attn (the BF1 forward of the
-default workload), attn_q0 (the same with Q = 0), gemm / gemm_zero (the
+default workload), attn_q0 (the same with Q = 0), dense (the in-house dense
+causal kernel on the same inputs), gemm / gemm_zero (the
 8192^3 bf16 matmul of mfma_reference on N(0,1) / all-zero operands).
 """
 
@@ -106,7 +107,7 @@ def parse():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-ttft", action="store_true")
     ap.add_argument("--no-gemm-ref", action="store_true")
-    ap.add_argument("--load", choices=["attn", "attn_q0", "gemm", "gemm_zero"], default=None,
+    ap.add_argument("--load", choices=["attn", "attn_q0", "dense", "gemm", "gemm_zero"], default=None,
                     help="run one workload back to back (see the module docstring) and exit")
     ap.add_argument("--load-seconds", type=float, default=8.0)
     ap.add_argument("--no-sweep-device", action="store_true",
@@ -248,7 +249,7 @@ def gemm_reference(torch, achieved, N=8192):
 def run_load(torch, bf1, synth, kind, seconds, workload):
     """One workload back to back for `seconds` (the --load mode): prints the
     number of calls and the device time per call."""
-    if kind.startswith("attn"):
+    if kind.startswith("attn") or kind == "dense":
         w = synth.WORKLOADS[workload]
         q, k, v = synth.make_qkv(w, device="cuda")
         if kind == "attn_q0":
@@ -257,6 +258,8 @@ def run_load(torch, bf1, synth, kind, seconds, workload):
         lse = torch.empty((w.batch, w.Hq, w.n), dtype=torch.float32, device="cuda")
         rp, ci = bf1.plan(w.n, w.b, w.L)
         fn = lambda: bf1.attn_fwd_csr(q, k, v, w.b, rp, ci, out=o, lse=lse)
+        if kind == "dense":
+            fn = lambda: bf1.dense_causal_fwd(q, k, v, out=o, lse=lse)
     else:
         N = 8192
         g = torch.Generator(device="cuda")
