@@ -69,7 +69,8 @@ two-order protocol and writes one JSON record per point to --sweep-out.
 and prints its time per call, nothing else (for sampling the GPU's shader
 clock from another process while it runs): attn (the BF1 forward of the
 default workload), attn_q0 (the same with Q = 0), dense (the in-house dense
-causal kernel on the same inputs), gemm / gemm_zero (the
+causal kernel on the same inputs), bwd (the backward of the BF1 forward on
+the same inputs), gemm / gemm_zero (the
 8192^3 bf16 matmul of mfma_reference on N(0,1) / all-zero operands).
 """
 
@@ -107,7 +108,7 @@ def parse():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-ttft", action="store_true")
     ap.add_argument("--no-gemm-ref", action="store_true")
-    ap.add_argument("--load", choices=["attn", "attn_q0", "dense", "gemm", "gemm_zero"], default=None,
+    ap.add_argument("--load", choices=["attn", "attn_q0", "dense", "bwd", "gemm", "gemm_zero"], default=None,
                     help="run one workload back to back (see the module docstring) and exit")
     ap.add_argument("--load-seconds", type=float, default=8.0)
     ap.add_argument("--no-sweep-device", action="store_true",
@@ -249,7 +250,7 @@ def gemm_reference(torch, achieved, N=8192):
 def run_load(torch, bf1, synth, kind, seconds, workload):
     """One workload back to back for `seconds` (the --load mode): prints the
     number of calls and the device time per call."""
-    if kind.startswith("attn") or kind == "dense":
+    if kind.startswith("attn") or kind in ("dense", "bwd"):
         w = synth.WORKLOADS[workload]
         q, k, v = synth.make_qkv(w, device="cuda")
         if kind == "attn_q0":
@@ -260,6 +261,15 @@ def run_load(torch, bf1, synth, kind, seconds, workload):
         fn = lambda: bf1.attn_fwd_csr(q, k, v, w.b, rp, ci, out=o, lse=lse)
         if kind == "dense":
             fn = lambda: bf1.dense_causal_fwd(q, k, v, out=o, lse=lse)
+        elif kind == "bwd":
+            fn()
+            do = synth.make_grad_out(w, device="cuda")
+            dq = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+            dk = torch.empty(k.shape, dtype=torch.float32, device="cuda")
+            dv = torch.empty_like(dk)
+            ws = torch.empty(bf1.bwd_workspace_size(w.batch, w.n, w.Hq, w.Hkv, w.d, w.b, w.L),
+                             dtype=torch.uint8, device="cuda")
+            fn = lambda: bf1.attn_bwd(q, k, v, o, do, lse, w.b, w.L, dq=dq, dk=dk, dv=dv, workspace=ws)
     else:
         N = 8192
         g = torch.Generator(device="cuda")
