@@ -67,3 +67,13 @@ def test_kernel_source_hash_is_stable():
     # the committed counter figure names the sources it was taken on; bench.py
     # reports it only while they match the tree
     assert len(t["kernel_source_sha256"]) == 64 and t["bytes_per_launch"] > 0
+
+
+def test_profiles_index_lists_every_summary():
+    # every committed profile summary is listed (with what it covers) in the index
+    pdir = os.path.join(ROOT, "profiles")
+    index = open(os.path.join(pdir, "README.md")).read()
+    for name in sorted(os.listdir(pdir)):
+        if name == "README.md":
+            continue
+        assert f"`{name}`" in index, name
